@@ -26,7 +26,10 @@ the lowest index winning ties, retirement by per-request stop length) are the
 published Llama-2 architecture, restated here in plain numpy.
 
 Everything is fp64.  Weights are the exact fp32 / bf16 values drawn by the
-counter-based generator in wgen.c, widened to fp64.
+counter-based generator in wgen.c, widened to fp64.  The KV cache is model
+state kept in the model's storage format: a key or value is rounded to bf16
+(fp32 for fp32 models), nearest-even, when it is cached, and attention reads
+the cached values.  Nothing else is rounded.
 
 Two forms of the same computation are provided:
   * ``forward_causal``  -- one causal pass over a whole token sequence, giving
@@ -63,6 +66,10 @@ class Shape:
     rope_base: float = 10000.0
     rms_eps: float = 1e-5
     bf16: bool = True
+    # Cached keys/values are stored in the model's storage format (bf16 or
+    # fp32), rounded to nearest-even when written.  False keeps them exact
+    # (fp64), which only the brute-force pins use.
+    kv_round: bool = True
 
     def matrix_dims(self, name: str):
         d, hd = self.d_model, self.head_dim
@@ -152,6 +159,23 @@ def apply_rope(x: np.ndarray, positions: Sequence[int], base: float) -> np.ndarr
     return out
 
 
+def round_to_storage(x: np.ndarray, bf16: bool) -> np.ndarray:
+    """Value of x once stored as fp32, or as bf16 (via fp32), round-to-nearest-even at each step."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    if bf16:
+        u = f.view(np.uint32).astype(np.uint64)
+        u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+        f = u.astype(np.uint32).view(np.float32)
+    return f.astype(np.float64)
+
+
+def cache_kv(shape: Shape, k: np.ndarray, v: np.ndarray):
+    """Keys/values as the KV cache holds them (the model's storage format)."""
+    if not shape.kv_round:
+        return k, v
+    return round_to_storage(k, shape.bf16), round_to_storage(v, shape.bf16)
+
+
 def softmax(s: np.ndarray) -> np.ndarray:
     """Softmax over the last axis, with the row max subtracted first."""
     m = np.max(s, axis=-1, keepdims=True)
@@ -239,6 +263,7 @@ def forward_causal(w: Weights, tokens: Sequence[int], want_positions: Optional[S
         v = (a @ W["wv"].T).reshape(T, sh.n_kv_heads, sh.head_dim)
         q = apply_rope(q, pos, sh.rope_base)
         k = apply_rope(k, pos, sh.rope_base)
+        k, v = cache_kv(sh, k, v)
         o = causal_attention(q, k, v).reshape(T, sh.n_heads * sh.head_dim)
         x = x + o @ W["wo"].T
         m = rmsnorm(x, g, sh.rms_eps)
@@ -310,6 +335,7 @@ class KVCacheDecoder:
             v = (a @ W["wv"].T).reshape(n, sh.n_kv_heads, sh.head_dim)
             q = apply_rope(q, positions, sh.rope_base)
             k = apply_rope(k, positions, sh.rope_base)
+            k, v = cache_kv(sh, k, v)
             for r in range(n):
                 self.K[rids[r]][layer][positions[r]] = k[r]
                 self.V[rids[r]][layer][positions[r]] = v[r]

@@ -1,0 +1,255 @@
+// Decode attention over the paged KV cache, one query position per row
+// (Section II-A: each new token attends to the cached keys and values of all
+// earlier tokens of its request, the directive prefix included).
+//
+// Work item = (KV split, row, KV head).  A workgroup of four waves walks the
+// 16-position blocks of its split, wave w taking every fourth block.  Per
+// block, on MFMA:
+//   S[t][h]  = K_tile(16 x hd) . Q^T(hd x 16)      -- t = position, h = query
+//              head of the KV group (G <= 16 columns used; grouped-query heads
+//              share the K/V tile they read once)
+//   online softmax over t (column-wise max with wavefront shuffles, exp2 of
+//   log2e-scaled scores)
+//   O^T[e][h] += V^T_tile(hd x 16) . P(16 x 16)   -- P is the S accumulator
+//              re-used in place as the B operand: no shuffle, no LDS
+// The four waves are merged through LDS (log-sum-exp), and a split's result
+// either is final (written as the O-projection input) or goes to a partial
+// buffer merged by k_attn_merge.
+// bf16 keys are multiplied by q split into hi + lo bf16 parts, so the scores
+// carry fp32-level precision of q.
+#pragma once
+
+#include "gemm_kernels.h"
+
+namespace sprk {
+
+struct AttnArgs {
+  const float* q;         // [rows][H][hd], fp32
+  const void* kc;         // this layer's K blocks [block][Hkv][16][hd]
+  const void* vc;         // this layer's V blocks [block][Hkv][hd][16]
+  const int32_t* bt;      // [slots][mb]
+  void* act;              // output, K-block-major over H * hd
+  float* part;            // [rows][H][kSplitsMax][hd + 4]: m, l, -, -, o[hd]
+  int n_rows, H, Hkv, G, mb, bps, Rp;
+  float qscale;           // log2(e) / sqrt(hd)
+  RowSlotPos rows;
+};
+
+__device__ __forceinline__ int attn_nsplit(int pos, int bps) {
+  const int nblk = (pos + 1 + 15) >> 4;
+  return (nblk + bps - 1) / bps;
+}
+
+// Four consecutive positions of one V^T row (one dimension), as loaded.
+template <class P>
+struct VQuad;
+template <>
+struct VQuad<BF16> {
+  uint2 raw;
+  __device__ __forceinline__ void load(const uint16_t* v) { raw = *reinterpret_cast<const uint2*>(v); }
+  // Positions past the context hold stale or never-written cache memory; they
+  // get probability 0, but 0 * NaN would still poison the sum, so zero them.
+  __device__ __forceinline__ void mask(int valid) {
+    if (valid <= 0) raw.x = 0u;
+    else if (valid == 1) raw.x &= 0xFFFFu;
+    if (valid <= 2) raw.y = 0u;
+    else if (valid == 3) raw.y &= 0xFFFFu;
+  }
+};
+template <>
+struct VQuad<F32> {
+  uint4 raw;
+  __device__ __forceinline__ void load(const float* v) { raw = *reinterpret_cast<const uint4*>(v); }
+  __device__ __forceinline__ void mask(int valid) {
+    if (valid <= 0) raw.x = 0u;
+    if (valid <= 1) raw.y = 0u;
+    if (valid <= 2) raw.z = 0u;
+    if (valid <= 3) raw.w = 0u;
+  }
+};
+
+// acc(16 dims x 16 heads) += V^T(16 dims x 16 positions) . P(16 positions x 16 heads).
+// bf16: the probabilities go in as hi + lo parts (two MFMAs).
+__device__ __forceinline__ f32x4_t mma_tok16(f32x4_t acc, const VQuad<BF16>& v, const float* p) {
+  const s16x4_t a = __builtin_bit_cast(s16x4_t, v.raw);
+  s16x4_t bh, bl;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint16_t h = f32_to_bf16_bits(p[r]);
+    bh[r] = static_cast<short>(h);
+    bl[r] = static_cast<short>(f32_to_bf16_bits(p[r] - bf16_bits_to_f32(h)));
+  }
+  acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4_t mma_tok16(f32x4_t acc, const VQuad<F32>& v, const float* p) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.x), p[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.y), p[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.z), p[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.w), p[3], acc, 0, 0, 0);
+  return acc;
+}
+
+template <class P, int HD>
+__global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
+  using E = typename P::elem;
+  constexpr bool kBf16 = sizeof(E) == 2;
+  constexpr int NF = HD * static_cast<int>(sizeof(E)) / 64;  // 16-byte fragments per lane per key row
+  constexpr int SEG = HD / 4;                                // dims per lane group
+  constexpr int NE = HD / 16;                                // 16-dim output chunks
+  const int s = blockIdx.x, b = blockIdx.y, kvh = blockIdx.z;
+  const int pos = a.rows.pos[b];
+  const int ctx = pos + 1;
+  const int nblk = (ctx + 15) >> 4;
+  const int nsplit = (nblk + a.bps - 1) / a.bps;
+  if (s >= nsplit) return;
+  const int lo = s * a.bps, hi = min(nblk, lo + a.bps);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane & 15, g = lane >> 4;
+  const bool hv = h < a.G;
+
+  // Q^T operand (hi and lo parts for bf16), scaled so scores are in log2 units.
+  uint4 qh[NF], ql[NF];
+  {
+    const float* qp = a.q + (static_cast<size_t>(b) * a.H + kvh * a.G + (hv ? h : 0)) * HD + g * SEG;
+#pragma unroll
+    for (int c = 0; c < NF; ++c) {
+      union {
+        uint4 u;
+        E e[P::per16];
+      } vh, vl;
+#pragma unroll
+      for (int j = 0; j < P::per16; ++j) {
+        const float v = hv ? qp[c * P::per16 + j] * a.qscale : 0.f;
+        vh.e[j] = P::from_f32(v);
+        vl.e[j] = P::from_f32(v - P::to_f32(vh.e[j]));
+      }
+      qh[c] = vh.u;
+      ql[c] = vl.u;
+    }
+  }
+
+  f32x4_t O[NE];
+#pragma unroll
+  for (int e = 0; e < NE; ++e) O[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const int32_t* btrow = a.bt + static_cast<size_t>(a.rows.slot[b]) * a.mb;
+  const E* kc = static_cast<const E*>(a.kc);
+  const E* vc = static_cast<const E*>(a.vc);
+
+  for (int i = lo + wave; i < hi; i += 4) {
+    const size_t tile = static_cast<size_t>(btrow[i]) * a.Hkv + kvh;
+    const uint4* kt = reinterpret_cast<const uint4*>(kc + (tile * 16 + (lane & 15)) * HD + g * SEG);
+    uint4 kf[NF];
+#pragma unroll
+    for (int c = 0; c < NF; ++c) kf[c] = kt[c];
+    const E* vt = vc + (tile * HD + (lane & 15)) * 16 + 4 * g;
+    VQuad<P> vq[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) vq[e].load(vt + e * 16 * 16);
+
+    f32x4_t S = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NF; ++c) {
+      S = P::mma(S, kf[c], qh[c]);
+      if constexpr (kBf16) S = P::mma(S, kf[c], ql[c]);
+    }
+    const int t0 = i * 16 + 4 * g;
+    if (t0 + 4 > ctx) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (t0 + r >= ctx) S[r] = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < NE; ++e) vq[e].mask(ctx - t0);
+    }
+    float mb = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
+    mb = fmaxf(mb, __shfl_xor(mb, 16));
+    mb = fmaxf(mb, __shfl_xor(mb, 32));
+    const float m_new = fmaxf(m_run, mb);
+    const float alpha = exp2f(m_run - m_new);
+    float p[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = exp2f(S[r] - m_new);
+    l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      O[e][0] *= alpha;
+      O[e][1] *= alpha;
+      O[e][2] *= alpha;
+      O[e][3] *= alpha;
+      O[e] = mma_tok16(O[e], vq[e], p);
+    }
+    m_run = m_new;
+  }
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+
+  __shared__ float sm[3][2 + 4 * NE][64];
+  if (wave > 0) {
+    sm[wave - 1][0][lane] = m_run;
+    sm[wave - 1][1][lane] = l_run;
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm[wave - 1][2 + 4 * e + r][lane] = O[e][r];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  float M = m_run;
+  for (int w = 0; w < 3; ++w) M = fmaxf(M, sm[w][0][lane]);
+  const float c0 = exp2f(m_run - M);
+  float L = l_run * c0;
+#pragma unroll
+  for (int e = 0; e < NE; ++e)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) O[e][r] *= c0;
+  for (int w = 0; w < 3; ++w) {
+    const float cw = exp2f(sm[w][0][lane] - M);
+    L += cw * sm[w][1][lane];
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) O[e][r] += cw * sm[w][2 + 4 * e + r][lane];
+  }
+  if (!hv) return;
+  const int hq = kvh * a.G + h;
+  if (nsplit == 1) {
+    const float inv = 1.f / L;
+    E* act = static_cast<E*>(a.act);
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+      store_act4<P>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
+                    O[e][3] * inv);
+  } else {
+    float* pp = a.part + ((static_cast<size_t>(b) * a.H + hq) * kSplitsMax + s) * (HD + 4);
+    if (g == 0) {
+      pp[0] = M;
+      pp[1] = L;
+    }
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+      *reinterpret_cast<float4*>(pp + 4 + 16 * e + 4 * g) = make_float4(O[e][0], O[e][1], O[e][2], O[e][3]);
+  }
+}
+
+// Log-sum-exp merge of the KV splits of rows that needed more than one.
+template <class P, int HD>
+__global__ __launch_bounds__(HD) void k_attn_merge(AttnArgs a) {
+  const int b = blockIdx.x, hq = blockIdx.y, dd = threadIdx.x;
+  const int nsplit = attn_nsplit(a.rows.pos[b], a.bps);
+  if (nsplit <= 1) return;
+  const float* pp = a.part + (static_cast<size_t>(b) * a.H + hq) * kSplitsMax * (HD + 4);
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pp[s * (HD + 4)]);
+  float L = 0.f, O = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float c = exp2f(pp[s * (HD + 4)] - M);
+    L += c * pp[s * (HD + 4) + 1];
+    O += c * pp[s * (HD + 4) + 4 + dd];
+  }
+  const int k = hq * HD + dd;
+  P::store_act(act_record<P>(static_cast<typename P::elem*>(a.act), a.Rp, b, k), k % P::kblk, O / L);
+}
+
+}  // namespace sprk

@@ -1,0 +1,142 @@
+// Device-side types and helpers for gfx950 (CDNA4): element formats, 16-byte
+// operand fragments and the MFMA forms the kernels use.
+//
+// Fragment convention (both dtypes): one MFMA operand fragment is 64 lanes x
+// 16 bytes.  Lane l = r + 16 g holds row (or column) r of a 16-wide tile and
+// the g-th quarter of a K-block: 8 bf16 or 4 fp32 elements.  A K-block is
+// therefore 32 bf16 or 16 fp32 elements.  Any consistent assignment of K
+// indices to (lane group, element) gives the same dot products, so the weight
+// tiles, the activation buffers and the attention K/V tiles only have to agree
+// with each other.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sprk {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));  // round to nearest even
+}
+
+// bf16 storage: 16-bit elements, 32 per K-block, MFMA 16x16x32.  An
+// activation (an MFMA B operand) is carried as two bf16 parts, hi = bf16(v)
+// and lo = bf16(v - hi), so the product with a bf16 weight keeps about 16
+// significant bits of the fp32 activation.
+struct BF16 {
+  using elem = uint16_t;
+  static constexpr int kblk = 32;
+  static constexpr int per16 = 8;   // elements per 16 bytes
+  static constexpr int parts = 2;   // activation parts (hi, lo)
+  static __device__ __forceinline__ elem from_f32(float f) { return f32_to_bf16_bits(f); }
+  static __device__ __forceinline__ float to_f32(elem e) { return bf16_bits_to_f32(e); }
+
+  // acc += A(16 x 32) * B(32 x 16) for one fragment pair.
+  static __device__ __forceinline__ f32x4_t mma(f32x4_t acc, uint4 a, uint4 b) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   acc, 0, 0, 0);
+  }
+  // Sum of squares of the activation values hi + lo of one fragment.
+  static __device__ __forceinline__ float sumsq(uint4 h, uint4 l) {
+    float s = 0.f;
+    const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
+    const uint32_t lw[4] = {l.x, l.y, l.z, l.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v0 = __uint_as_float(hw[i] << 16) + __uint_as_float(lw[i] << 16);
+      const float v1 = __uint_as_float(hw[i] & 0xFFFF0000u) + __uint_as_float(lw[i] & 0xFFFF0000u);
+      s = fmaf(v0, v0, s);
+      s = fmaf(v1, v1, s);
+    }
+    return s;
+  }
+  // Writes activation value v at element kk of the (K-block, row) record `rec`.
+  static __device__ __forceinline__ void store_act(elem* rec, int kk, float v) {
+    const elem hi = from_f32(v);
+    rec[kk] = hi;
+    rec[kblk + kk] = from_f32(v - to_f32(hi));
+  }
+};
+
+// fp32 storage: 16 elements per K-block, four MFMA 16x16x4 per fragment pair.
+struct F32 {
+  using elem = float;
+  static constexpr int kblk = 16;
+  static constexpr int per16 = 4;
+  static constexpr int parts = 1;
+  static __device__ __forceinline__ elem from_f32(float f) { return f; }
+  static __device__ __forceinline__ float to_f32(elem e) { return e; }
+
+  static __device__ __forceinline__ f32x4_t mma(f32x4_t acc, uint4 a, uint4 b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    return acc;
+  }
+  static __device__ __forceinline__ float sumsq(uint4 v, uint4) {
+    float s = 0.f;
+    s = fmaf(__uint_as_float(v.x), __uint_as_float(v.x), s);
+    s = fmaf(__uint_as_float(v.y), __uint_as_float(v.y), s);
+    s = fmaf(__uint_as_float(v.z), __uint_as_float(v.z), s);
+    s = fmaf(__uint_as_float(v.w), __uint_as_float(v.w), s);
+    return s;
+  }
+  static __device__ __forceinline__ void store_act(elem* rec, int kk, float v) { rec[kk] = v; }
+};
+
+// Activation buffers are K-block-major: the record of (K-block kb, row b)
+// holds P::parts runs of kblk elements (64 bytes each) and sits at element
+// offset (kb * Rp + b) * parts * kblk.
+template <class P>
+__device__ __forceinline__ typename P::elem* act_record(typename P::elem* act, int Rp, int b, int k) {
+  return act + (static_cast<size_t>(k / P::kblk) * Rp + b) * (P::parts * P::kblk);
+}
+
+// ---------------------------------------------------------------------------
+// Counter-based N(0, 0.02) weight draw.  SplitMix64 (Steele, Lea, Flood,
+// OOPSLA 2014): the n-th output of a stream seeded with s is
+// mix(s + n * 0x9E3779B97F4A7C15).  A matrix (tensor t, layer l) uses the
+// stream whose seed is output 1 + 256 t + l of the stream seeded with the
+// model seed; its element with row-major index e sums the eight 16-bit lanes
+// of outputs 2e+1 and 2e+2 (an Irwin-Hall sum with mean 262140), and the
+// weight is fp32(sum - 262140) * 0x1.91530cp-22 (std 0.02), rounded to the
+// storage format.  Integer steps and one IEEE multiply: bit-exact anywhere.
+// ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ uint64_t sm_mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__host__ __device__ __forceinline__ uint64_t sm_output(uint64_t seed, uint64_t n) {
+  return sm_mix64(seed + n * 0x9E3779B97F4A7C15ull);
+}
+
+__device__ __forceinline__ uint32_t lanes16_sum(uint64_t r) {
+  return static_cast<uint32_t>(r & 0xFFFF) + static_cast<uint32_t>((r >> 16) & 0xFFFF) +
+         static_cast<uint32_t>((r >> 32) & 0xFFFF) + static_cast<uint32_t>(r >> 48);
+}
+
+__device__ __forceinline__ float weight_draw(uint64_t stream, uint64_t e) {
+  const uint32_t s = lanes16_sum(sm_output(stream, 2 * e + 1)) + lanes16_sum(sm_output(stream, 2 * e + 2));
+  return static_cast<float>(static_cast<int32_t>(s) - 262140) * 0x1.91530cp-22f;
+}
+
+template <class P>
+__device__ __forceinline__ typename P::elem weight_elem(uint64_t stream, uint64_t e) {
+  return P::from_f32(weight_draw(stream, e));
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+}  // namespace sprk

@@ -1,0 +1,270 @@
+// Host-side bookkeeping of the decode model (see host_state.h).
+#include "host_state.h"
+
+#include <cmath>
+#include <limits>
+
+namespace spr {
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+bool fail(std::string* err, const std::string& msg) {
+  if (err) *err = msg;
+  return false;
+}
+
+}  // namespace
+
+bool derive(const spr_config& c, Dims* out, std::string* err) {
+  if (c.n_layers < 1 || c.n_layers > 255) return fail(err, "n_layers must be in [1, 255]");
+  if (c.head_dim != 64 && c.head_dim != 128) return fail(err, "head_dim must be 64 or 128");
+  if (c.n_heads < 1 || c.n_kv_heads < 1 || c.n_heads % c.n_kv_heads != 0)
+    return fail(err, "n_heads must be a positive multiple of n_kv_heads");
+  if (c.n_heads / c.n_kv_heads > 16) return fail(err, "n_heads / n_kv_heads must be <= 16");
+  if (c.d_model < 16 || c.d_model % 16 != 0) return fail(err, "d_model must be a positive multiple of 16");
+  if (c.d_ff < 1 || c.vocab < 1) return fail(err, "d_ff and vocab must be >= 1");
+  if (c.dtype != SPR_F32 && c.dtype != SPR_BF16) return fail(err, "dtype must be SPR_F32 or SPR_BF16");
+  if (c.kv_block != kKvBlock) return fail(err, "kv_block must be 16");
+  if (c.max_slots < 1 || c.max_slots > 64) return fail(err, "max_slots must be in [1, 64]");
+  if (c.max_ctx < 1 || c.max_ctx > (1 << 20)) return fail(err, "max_ctx must be in [1, 2^20]");
+  if (c.kv_blocks < 1) return fail(err, "kv_blocks must be >= 1");
+  if (!(c.rope_base > 0.0f) || !std::isfinite(c.rope_base)) return fail(err, "rope_base must be positive");
+  if (!(c.rms_eps >= 0.0f) || !std::isfinite(c.rms_eps)) return fail(err, "rms_eps must be >= 0");
+  if (static_cast<int64_t>(c.n_heads) * c.head_dim > (1 << 20) || c.d_ff > (1 << 24) || c.d_model > (1 << 20) ||
+      c.vocab > (1 << 24))
+    return fail(err, "dimension too large");
+  Dims d{};
+  d.L = c.n_layers;
+  d.d = c.d_model;
+  d.H = c.n_heads;
+  d.Hkv = c.n_kv_heads;
+  d.hd = c.head_dim;
+  d.f = c.d_ff;
+  d.V = c.vocab;
+  d.G = c.n_heads / c.n_kv_heads;
+  d.dtype = c.dtype;
+  d.esize = c.dtype == SPR_BF16 ? 2 : 4;
+  d.kblk = c.dtype == SPR_BF16 ? 32 : 16;
+  d.qkv_rows = (d.H + 2 * d.Hkv) * d.hd;
+  d.o_in = d.H * d.hd;
+  d.nt_qkv = d.qkv_rows / 16;
+  d.nt_o = d.d / 16;
+  d.nt_13 = ceil_div(d.f, 8);
+  d.nt_2 = d.d / 16;
+  d.nt_lm = ceil_div(d.V, 16);
+  d.kb_d = ceil_div(d.d, d.kblk);
+  d.kb_o = ceil_div(d.o_in, d.kblk);
+  d.kb_f = ceil_div(d.f, d.kblk);
+  d.kb_max = d.kb_d;
+  if (d.kb_o > d.kb_max) d.kb_max = d.kb_o;
+  if (d.kb_f > d.kb_max) d.kb_max = d.kb_f;
+  d.S = c.max_slots;
+  d.max_ctx = c.max_ctx;
+  d.mb = ceil_div(c.max_ctx, kKvBlock);
+  d.nb = c.kv_blocks;
+  d.rope_base = c.rope_base;
+  d.eps = c.rms_eps;
+  *out = d;
+  return true;
+}
+
+Layout layout(const Dims& d) {
+  Layout l{};
+  const size_t F = kFragBytes;
+  l.wqkv = align256(static_cast<size_t>(d.nt_qkv) * d.kb_d * F);
+  l.wo = align256(static_cast<size_t>(d.nt_o) * d.kb_o * F);
+  l.w13 = align256(static_cast<size_t>(d.nt_13) * d.kb_d * F);
+  l.w2 = align256(static_cast<size_t>(d.nt_2) * d.kb_f * F);
+  size_t off = 0;
+  auto take = [&off](size_t bytes) {
+    size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  l.off_wqkv = take(l.wqkv * d.L);
+  l.off_wo = take(l.wo * d.L);
+  l.off_w13 = take(l.w13 * d.L);
+  l.off_w2 = take(l.w2 * d.L);
+  l.off_wlm = take(static_cast<size_t>(d.nt_lm) * d.kb_d * F);
+  l.off_emb = take(static_cast<size_t>(d.V) * d.d * d.esize);
+  l.off_rope = take(static_cast<size_t>(d.max_ctx) * (d.hd / 2) * 2 * sizeof(float));
+  l.kv_layer_stride = static_cast<size_t>(d.nb) * d.Hkv * kKvBlock * d.hd * d.esize;
+  l.off_kc = take(l.kv_layer_stride * d.L);
+  l.off_vc = take(l.kv_layer_stride * d.L);
+  l.off_bt = take(static_cast<size_t>(d.S) * d.mb * sizeof(int32_t));
+  l.off_x = take(static_cast<size_t>(kMaxRows) * d.d * sizeof(float));
+  // Activation records carry hi + lo parts for bf16 models.
+  l.act_bytes = static_cast<size_t>(d.kb_max) * kMaxRows * d.kblk * d.esize * (d.dtype == SPR_BF16 ? 2 : 1);
+  l.off_act0 = take(l.act_bytes);
+  l.off_act1 = take(l.act_bytes);
+  l.off_q = take(static_cast<size_t>(kMaxRows) * d.H * d.hd * sizeof(float));
+  l.off_part = take(static_cast<size_t>(kMaxRows) * d.H * kMaxSplits * (d.hd + 4) * sizeof(float));
+  l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
+  l.total = off;
+  return l;
+}
+
+void SlotTable::init(const Dims& d) {
+  d_ = d;
+  slots_.assign(d.S, Slot{});
+  free_.clear();
+  free_.reserve(d.nb);
+  for (int b = d.nb - 1; b >= 0; --b) free_.push_back(b);  // block 0 is handed out first
+}
+
+spr_status SlotTable::check_prefill(int n, const int32_t* slots, const int32_t* seq_lens, const int32_t* stop_lens,
+                                    std::string* err) const {
+  if (n < 1 || n > d_.S) {
+    *err = "prefill: n must be in [1, max_slots]";
+    return SPR_ERR_INVALID_ARG;
+  }
+  std::vector<char> seen(d_.S, 0);
+  int64_t need = 0;
+  for (int i = 0; i < n; ++i) {
+    const int s = slots[i];
+    if (s < 0 || s >= d_.S) {
+      *err = "prefill: slot id out of range";
+      return SPR_ERR_INVALID_ARG;
+    }
+    if (seen[s]) {
+      *err = "prefill: slot listed twice";
+      return SPR_ERR_INVALID_ARG;
+    }
+    seen[s] = 1;
+    if (slots_[s].state != kFree) {
+      *err = "prefill: slot " + std::to_string(s) + " is not free";
+      return SPR_ERR_STATE;
+    }
+    if (seq_lens[i] < 1 || stop_lens[i] < 1) {
+      *err = "prefill: seq_len and stop_len must be >= 1";
+      return SPR_ERR_INVALID_ARG;
+    }
+    const int64_t positions = static_cast<int64_t>(seq_lens[i]) + stop_lens[i] - 1;
+    if (positions > d_.max_ctx) {
+      *err = "prefill: seq_len + stop_len - 1 exceeds max_ctx";
+      return SPR_ERR_INVALID_ARG;
+    }
+    need += (positions + kKvBlock - 1) / kKvBlock;
+  }
+  if (need > static_cast<int64_t>(free_.size())) {
+    *err = "prefill: KV pool has " + std::to_string(free_.size()) + " free blocks, " + std::to_string(need) +
+           " needed";
+    return SPR_ERR_KV_FULL;
+  }
+  return SPR_OK;
+}
+
+void SlotTable::commit_prefill(int n, const int32_t* slots, const int32_t* seq_lens, const int32_t* stop_lens,
+                               int32_t* retired) {
+  for (int i = 0; i < n; ++i) {
+    Slot& sl = slots_[slots[i]];
+    const int positions = seq_lens[i] + stop_lens[i] - 1;
+    const int nblk = (positions + kKvBlock - 1) / kKvBlock;
+    sl.blocks.clear();
+    for (int b = 0; b < nblk; ++b) {
+      sl.blocks.push_back(free_.back());
+      free_.pop_back();
+    }
+    sl.len = seq_lens[i];
+    sl.produced = 1;
+    sl.stop = stop_lens[i];
+    sl.state = sl.produced >= sl.stop ? kFinished : kActive;
+    if (retired) retired[i] = sl.state == kFinished ? 1 : 0;
+  }
+}
+
+spr_status SlotTable::check_decode(int n, const int32_t* slots, const int32_t* lens, std::string* err) const {
+  if (n < 1 || n > d_.S) {
+    *err = "decode_step: n_active must be in [1, max_slots]";
+    return SPR_ERR_INVALID_ARG;
+  }
+  std::vector<char> seen(d_.S, 0);
+  for (int i = 0; i < n; ++i) {
+    const int s = slots[i];
+    if (s < 0 || s >= d_.S) {
+      *err = "decode_step: slot id out of range";
+      return SPR_ERR_INVALID_ARG;
+    }
+    if (seen[s]) {
+      *err = "decode_step: slot listed twice";
+      return SPR_ERR_INVALID_ARG;
+    }
+    seen[s] = 1;
+    const Slot& sl = slots_[s];
+    if (sl.state != kActive) {
+      *err = "decode_step: slot " + std::to_string(s) + (sl.state == kFree ? " is free" : " has finished");
+      return SPR_ERR_STATE;
+    }
+    if (lens[i] != sl.len) {
+      *err = "decode_step: slot " + std::to_string(s) + " has " + std::to_string(sl.len) + " cached positions, " +
+             std::to_string(lens[i]) + " given";
+      return SPR_ERR_STATE;
+    }
+  }
+  return SPR_OK;
+}
+
+void SlotTable::commit_decode(int n, const int32_t* slots, int32_t* retired) {
+  for (int i = 0; i < n; ++i) {
+    Slot& sl = slots_[slots[i]];
+    sl.len += 1;
+    sl.produced += 1;
+    const bool done = sl.produced >= sl.stop;
+    if (done) sl.state = kFinished;
+    if (retired) retired[i] = done ? 1 : 0;
+  }
+}
+
+spr_status SlotTable::check_rewind(int slot, int len, int produced, std::string* err) const {
+  if (slot < 0 || slot >= d_.S) {
+    *err = "rewind: slot id out of range";
+    return SPR_ERR_INVALID_ARG;
+  }
+  const Slot& sl = slots_[slot];
+  if (sl.state == kFree) {
+    *err = "rewind: slot is free";
+    return SPR_ERR_STATE;
+  }
+  const int prompt = sl.len - sl.produced + 1;
+  if (produced < 1 || produced > sl.produced || len != prompt + produced - 1) {
+    *err = "rewind: need 1 <= produced <= current and len == prompt + produced - 1";
+    return SPR_ERR_INVALID_ARG;
+  }
+  return SPR_OK;
+}
+
+void SlotTable::commit_rewind(int slot, int len, int produced) {
+  Slot& sl = slots_[slot];
+  sl.len = len;
+  sl.produced = produced;
+  sl.state = produced >= sl.stop ? kFinished : kActive;
+}
+
+spr_status SlotTable::check_free(int slot, std::string* err) const {
+  if (slot < 0 || slot >= d_.S) {
+    *err = "free_slot: slot id out of range";
+    return SPR_ERR_INVALID_ARG;
+  }
+  if (slots_[slot].state == kFree) {
+    *err = "free_slot: slot is already free";
+    return SPR_ERR_STATE;
+  }
+  return SPR_OK;
+}
+
+void SlotTable::commit_free(int slot) {
+  Slot& sl = slots_[slot];
+  for (auto it = sl.blocks.rbegin(); it != sl.blocks.rend(); ++it) free_.push_back(*it);
+  sl = Slot{};
+}
+
+void SlotTable::block_row(int slot, int32_t* row) const {
+  const Slot& sl = slots_[slot];
+  for (int b = 0; b < d_.mb; ++b) row[b] = b < static_cast<int>(sl.blocks.size()) ? sl.blocks[b] : 0;
+}
+
+}  // namespace spr

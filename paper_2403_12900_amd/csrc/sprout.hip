@@ -1,0 +1,570 @@
+// C ABI of the decode library (include/sprout.h): argument validation, the
+// host-side slot table, and the launch sequence of one forward pass over a
+// set of token rows.
+//
+// One forward pass (a decode step, or one prefill chunk of up to 128 token
+// rows) enqueues on the model's stream:
+//   k_embed                      token rows -> fp32 residual x, activation
+//   per layer:
+//     k_stream_gemm<EpiQKV>      RMSNorm . Wqkv, RoPE, q out, k/v appended to the paged cache
+//     k_attn_decode (+merge)     softmax(q K^T / sqrt(hd)) V over the row's cached positions
+//     k_stream_gemm<EpiResid>    x += o Wo^T
+//     k_stream_gemm<EpiSwiGLU>   h = SiLU(RMSNorm(x) W1^T) * (RMSNorm(x) W3^T)
+//     k_stream_gemm<EpiResid>    x += h W2^T
+//   k_stream_gemm<EpiLogits>     RMSNorm(x) Wlm^T, per-tile greedy candidates
+//   k_argmax_final               tok[slot] = lowest index of the row maximum
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "attn_kernels.h"
+#include "gemm_kernels.h"
+#include "host_state.h"
+#include "step_kernels.h"
+#include "wgen_kernels.h"
+
+using namespace sprk;
+
+struct spr_model {
+  spr::Dims d{};
+  spr::Layout lay{};
+  char* ws = nullptr;
+  hipStream_t st = nullptr;
+  spr::SlotTable tab;
+  std::vector<int32_t> bt_row;
+  bool sticky = false;
+  uint64_t seed = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+spr_status fail(spr_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+spr_status hip_fail(spr_model* m, const char* what, hipError_t e) {
+  if (m) m->sticky = true;
+  return fail(SPR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define SPR_HIP(m, expr)                               \
+  do {                                                 \
+    hipError_t e_ = (expr);                            \
+    if (e_ != hipSuccess) return hip_fail(m, #expr, e_); \
+  } while (0)
+
+#define SPR_LAUNCHED(m, what)                          \
+  do {                                                 \
+    hipError_t e_ = hipGetLastError();                 \
+    if (e_ != hipSuccess) return hip_fail(m, what, e_); \
+  } while (0)
+
+uint64_t stream_key(uint64_t seed, int tensor, int layer) {
+  return sm_output(seed, 1u + 256u * static_cast<uint64_t>(tensor) + static_cast<uint64_t>(layer));
+}
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+unsigned grid1(int64_t threads) { return static_cast<unsigned>((threads + 255) / 256); }
+
+MatSpec mat_spec(const spr::Dims& d, int kind, int layer, uint64_t seed) {
+  MatSpec s{};
+  s.kind = kind;
+  s.H = d.H;
+  s.Hkv = d.Hkv;
+  s.hd = d.hd;
+  s.f = d.f;
+  s.d = d.d;
+  s.V = d.V;
+  switch (kind) {
+    case MK_QKV:
+      s.NT = d.nt_qkv; s.KB = d.kb_d; s.K = d.d;
+      s.key[0] = stream_key(seed, 1, layer);
+      s.key[1] = stream_key(seed, 2, layer);
+      s.key[2] = stream_key(seed, 3, layer);
+      break;
+    case MK_O:
+      s.NT = d.nt_o; s.KB = d.kb_o; s.K = d.o_in;
+      s.key[0] = stream_key(seed, 4, layer);
+      break;
+    case MK_W13:
+      s.NT = d.nt_13; s.KB = d.kb_d; s.K = d.d;
+      s.key[0] = stream_key(seed, 5, layer);
+      s.key[1] = stream_key(seed, 6, layer);
+      break;
+    case MK_W2:
+      s.NT = d.nt_2; s.KB = d.kb_f; s.K = d.f;
+      s.key[0] = stream_key(seed, 7, layer);
+      break;
+    default:
+      s.NT = d.nt_lm; s.KB = d.kb_d; s.K = d.d;
+      s.key[0] = stream_key(seed, 8, 0);
+  }
+  return s;
+}
+
+struct Ptrs {
+  char* ws;
+  const spr::Layout* l;
+  char* wqkv(int layer) const { return ws + l->off_wqkv + l->wqkv * layer; }
+  char* wo(int layer) const { return ws + l->off_wo + l->wo * layer; }
+  char* w13(int layer) const { return ws + l->off_w13 + l->w13 * layer; }
+  char* w2(int layer) const { return ws + l->off_w2 + l->w2 * layer; }
+  char* wlm() const { return ws + l->off_wlm; }
+  char* emb() const { return ws + l->off_emb; }
+  char* kc(int layer) const { return ws + l->off_kc + l->kv_layer_stride * layer; }
+  char* vc(int layer) const { return ws + l->off_vc + l->kv_layer_stride * layer; }
+  int32_t* bt() const { return reinterpret_cast<int32_t*>(ws + l->off_bt); }
+  float* x() const { return reinterpret_cast<float*>(ws + l->off_x); }
+  char* act(int i) const { return ws + (i == 0 ? l->off_act0 : l->off_act1); }
+  float* q() const { return reinterpret_cast<float*>(ws + l->off_q); }
+  float* part() const { return reinterpret_cast<float*>(ws + l->off_part); }
+  float2* amax() const { return reinterpret_cast<float2*>(ws + l->off_amax); }
+  float2* rope() const { return reinterpret_cast<float2*>(ws + l->off_rope); }
+};
+
+template <class P>
+spr_status init_weights(spr_model* m) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  auto tiled = [&](char* dst, int kind, int layer) -> spr_status {
+    const MatSpec s = mat_spec(d, kind, layer, m->seed);
+    const int64_t threads = static_cast<int64_t>(s.NT) * s.KB * 64;
+    k_init_tiled<P><<<grid1(threads), 256, 0, m->st>>>(reinterpret_cast<uint4*>(dst), s);
+    SPR_LAUNCHED(m, "k_init_tiled");
+    return SPR_OK;
+  };
+  spr_status st;
+  for (int l = 0; l < d.L; ++l) {
+    if ((st = tiled(p.wqkv(l), MK_QKV, l)) != SPR_OK) return st;
+    if ((st = tiled(p.wo(l), MK_O, l)) != SPR_OK) return st;
+    if ((st = tiled(p.w13(l), MK_W13, l)) != SPR_OK) return st;
+    if ((st = tiled(p.w2(l), MK_W2, l)) != SPR_OK) return st;
+  }
+  if ((st = tiled(p.wlm(), MK_LM, 0)) != SPR_OK) return st;
+  const int64_t ne = static_cast<int64_t>(d.V) * d.d;
+  k_init_rowmajor<P><<<grid1(ne), 256, 0, m->st>>>(reinterpret_cast<typename P::elem*>(p.emb()), ne,
+                                                    stream_key(m->seed, 0, 0));
+  SPR_LAUNCHED(m, "k_init_rowmajor");
+  return SPR_OK;
+}
+
+// Rows of one forward pass.
+struct RowSet {
+  int n = 0;
+  int slot[kRows];
+  int pos[kRows];
+  int out_row[kRows];
+  int tok[kRows];
+};
+
+template <class P, class Epi>
+spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int KB, int JT, const Epi& epi) {
+  const uint4* w = reinterpret_cast<const uint4*>(W);
+  const uint4* x = reinterpret_cast<const uint4*>(X);
+  const int Rp = 16 * JT;
+  const bool wide = NT >= 512 || JT >= 8;  // 8-wave variants of JT = 8 would spill
+#define SPR_GEMM_CASE(JTV)                                                                         \
+  case JTV:                                                                                        \
+    if (wide)                                                                                      \
+      k_stream_gemm<P, JTV, 4, Epi><<<NT, 256, 0, m->st>>>(w, x, KB, Rp, epi.n_rows, epi);          \
+    else                                                                                           \
+      k_stream_gemm<P, JTV, 8, Epi><<<NT, 512, 0, m->st>>>(w, x, KB, Rp, epi.n_rows, epi);          \
+    break;
+  switch (JT) {
+    SPR_GEMM_CASE(1)
+    SPR_GEMM_CASE(2)
+    SPR_GEMM_CASE(4)
+    SPR_GEMM_CASE(8)
+    default:
+      return fail(SPR_ERR_INVALID_ARG, "internal: unsupported row-tile count");
+  }
+#undef SPR_GEMM_CASE
+  SPR_LAUNCHED(m, "k_stream_gemm");
+  return SPR_OK;
+}
+
+template <class P, int HD>
+spr_status launch_attention(spr_model* m, const AttnArgs& a, int max_splits) {
+  dim3 grid(max_splits, a.n_rows, a.Hkv);
+  k_attn_decode<P, HD><<<grid, 256, 0, m->st>>>(a);
+  SPR_LAUNCHED(m, "k_attn_decode");
+  if (max_splits > 1) {
+    k_attn_merge<P, HD><<<dim3(a.n_rows, a.H), HD, 0, m->st>>>(a);
+    SPR_LAUNCHED(m, "k_attn_merge");
+  }
+  return SPR_OK;
+}
+
+// One forward pass over rs (rows: slot, position, emitted logits row).
+// tok_in != null: the inputs are tok_in[slot]; otherwise rs.tok.  Emitting
+// rows write their greedy token to tok_out[slot].
+template <class P>
+spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
+                   bool do_lm) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  const int n = rs.n;
+  const int JT = n <= 16 ? 1 : n <= 32 ? 2 : n <= 64 ? 4 : 8;
+  const int Rp = 16 * JT;
+  using E = typename P::elem;
+  RowSlotPos sp;
+  std::memcpy(sp.slot, rs.slot, sizeof(sp.slot));
+  std::memcpy(sp.pos, rs.pos, sizeof(sp.pos));
+
+  {
+    EmbedArgs ea{};
+    ea.emb = p.emb();
+    ea.tok_dev = tok_in;
+    ea.x = p.x();
+    ea.act = p.act(0);
+    ea.n_rows = n;
+    ea.d = d.d;
+    ea.V = d.V;
+    ea.Rp = Rp;
+    std::memcpy(ea.slot, rs.slot, sizeof(ea.slot));
+    std::memcpy(ea.tok, rs.tok, sizeof(ea.tok));
+    k_embed<P><<<dim3(ceil_div(d.d / 4, 64), n), 64, 0, m->st>>>(ea);
+    SPR_LAUNCHED(m, "k_embed");
+  }
+
+  // KV splits: enough (row, head, split) work-groups to cover the chip.
+  int total_blk = 0, max_blk = 0;
+  for (int r = 0; r < n; ++r) {
+    const int nb = (rs.pos[r] + 1 + 15) / 16;
+    total_blk += nb;
+    if (nb > max_blk) max_blk = nb;
+  }
+  int bps = ceil_div(total_blk * d.Hkv, 1024);
+  if (bps < 4) bps = 4;
+  if (ceil_div(max_blk, bps) > kSplitsMax) bps = ceil_div(max_blk, kSplitsMax);
+  const int max_splits = ceil_div(max_blk, bps);
+
+  spr_status st;
+  for (int l = 0; l < d.L; ++l) {
+    {
+      EpiQKV<P> e{};
+      e.n_rows = n;
+      e.H = d.H;
+      e.Hkv = d.Hkv;
+      e.hd = d.hd;
+      e.mb = d.mb;
+      e.dnorm = d.d;
+      e.eps = d.eps;
+      e.q = p.q();
+      e.kc = reinterpret_cast<E*>(p.kc(l));
+      e.vc = reinterpret_cast<E*>(p.vc(l));
+      e.bt = p.bt();
+      e.rope = p.rope();
+      e.rows = sp;
+      if ((st = launch_gemm<P>(m, d.nt_qkv, p.wqkv(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
+    }
+    {
+      AttnArgs a{};
+      a.q = p.q();
+      a.kc = p.kc(l);
+      a.vc = p.vc(l);
+      a.bt = p.bt();
+      a.act = p.act(1);
+      a.part = p.part();
+      a.n_rows = n;
+      a.H = d.H;
+      a.Hkv = d.Hkv;
+      a.G = d.G;
+      a.mb = d.mb;
+      a.bps = bps;
+      a.Rp = Rp;
+      a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
+      a.rows = sp;
+      st = d.hd == 128 ? launch_attention<P, 128>(m, a, max_splits) : launch_attention<P, 64>(m, a, max_splits);
+      if (st != SPR_OK) return st;
+    }
+    {
+      EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      if ((st = launch_gemm<P>(m, d.nt_o, p.wo(l), p.act(1), d.kb_o, JT, e)) != SPR_OK) return st;
+    }
+    {
+      EpiSwiGLU<P> e{n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(1))};
+      if ((st = launch_gemm<P>(m, d.nt_13, p.w13(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
+    }
+    {
+      EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e)) != SPR_OK) return st;
+    }
+  }
+  if (!do_lm) return SPR_OK;
+  {
+    EpiLogits<P> e{};
+    e.n_rows = n;
+    e.V = d.V;
+    e.dnorm = d.d;
+    e.eps = d.eps;
+    e.logits = logits;
+    e.part = p.amax();
+    std::memcpy(e.out_row, rs.out_row, sizeof(e.out_row));
+    if ((st = launch_gemm<P>(m, d.nt_lm, p.wlm(), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
+  }
+  {
+    ArgmaxArgs a{};
+    a.part = p.amax();
+    a.tok_dev = tok_out;
+    a.n_tiles = d.nt_lm;
+    std::memcpy(a.slot, rs.slot, sizeof(a.slot));
+    std::memcpy(a.out_row, rs.out_row, sizeof(a.out_row));
+    k_argmax_final<<<n, 256, 0, m->st>>>(a);
+    SPR_LAUNCHED(m, "k_argmax_final");
+  }
+  return SPR_OK;
+}
+
+spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
+                       bool do_lm) {
+  return m->d.dtype == SPR_BF16 ? forward<BF16>(m, rs, tok_in, tok_out, logits, do_lm)
+                                : forward<F32>(m, rs, tok_in, tok_out, logits, do_lm);
+}
+
+spr_status check_model(const spr_model* m) {
+  if (m == nullptr) return fail(SPR_ERR_INVALID_ARG, "model is null");
+  if (m->sticky) return fail(SPR_ERR_HIP, "an earlier HIP error left the model unusable; release it");
+  return SPR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t spr_workspace_bytes(const spr_config* cfg) {
+  if (cfg == nullptr) return 0;
+  spr::Dims d;
+  std::string err;
+  if (!spr::derive(*cfg, &d, &err)) return 0;
+  return spr::layout(d).total;
+}
+
+spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t ws_bytes, void* hip_stream,
+                    spr_model** out) {
+  g_err.clear();
+  if (cfg == nullptr || out == nullptr) return fail(SPR_ERR_INVALID_ARG, "init: cfg and out must not be null");
+  *out = nullptr;
+  spr::Dims d;
+  std::string err;
+  if (!spr::derive(*cfg, &d, &err)) return fail(SPR_ERR_INVALID_ARG, "init: " + err);
+  const spr::Layout lay = spr::layout(d);
+  if (dev_ws == nullptr || (reinterpret_cast<uintptr_t>(dev_ws) & 255) != 0)
+    return fail(SPR_ERR_WORKSPACE, "init: workspace must be a non-null, 256-byte aligned device pointer");
+  if (ws_bytes < lay.total)
+    return fail(SPR_ERR_WORKSPACE, "init: workspace has " + std::to_string(ws_bytes) + " bytes, " +
+                                       std::to_string(lay.total) + " needed");
+  spr_model* m = new spr_model();
+  m->d = d;
+  m->lay = lay;
+  m->ws = static_cast<char*>(dev_ws);
+  m->st = static_cast<hipStream_t>(hip_stream);
+  m->seed = seed;
+  m->tab.init(d);
+  m->bt_row.assign(d.mb, 0);
+  spr_status st = d.dtype == SPR_BF16 ? init_weights<BF16>(m) : init_weights<F32>(m);
+  if (st != SPR_OK) {
+    delete m;
+    return st;
+  }
+  Ptrs p{m->ws, &m->lay};
+  // RoPE table: angle = pos * base^(-2i/hd), evaluated in double, stored as fp32 (cos, sin).
+  std::vector<float> rope(static_cast<size_t>(d.max_ctx) * d.hd);
+  for (int pos = 0; pos < d.max_ctx; ++pos)
+    for (int i = 0; i < d.hd / 2; ++i) {
+      const double theta = std::pow(static_cast<double>(d.rope_base), -2.0 * i / d.hd);
+      const double ang = pos * theta;
+      rope[(static_cast<size_t>(pos) * (d.hd / 2) + i) * 2] = static_cast<float>(std::cos(ang));
+      rope[(static_cast<size_t>(pos) * (d.hd / 2) + i) * 2 + 1] = static_cast<float>(std::sin(ang));
+    }
+  hipError_t e = hipMemcpyAsync(p.rope(), rope.data(), rope.size() * sizeof(float), hipMemcpyHostToDevice, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.bt(), 0, static_cast<size_t>(d.S) * d.mb * sizeof(int32_t), m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.act(0), 0, lay.act_bytes, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.act(1), 0, lay.act_bytes, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kMaxRows) * d.d * sizeof(float), m->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(m->st);
+  if (e != hipSuccess) {
+    hip_fail(nullptr, "init", e);
+    delete m;
+    return SPR_ERR_HIP;
+  }
+  *out = m;
+  return SPR_OK;
+}
+
+spr_status spr_prefill(spr_model* m, int32_t n, const int32_t* slots, const int32_t* tokens, const int32_t* seq_lens,
+                       const int32_t* stop_lens, int32_t* tok, float* logits, int32_t* retired) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (slots == nullptr || tokens == nullptr || seq_lens == nullptr || stop_lens == nullptr || tok == nullptr)
+    return fail(SPR_ERR_INVALID_ARG, "prefill: slots, tokens, seq_lens, stop_lens and tok must not be null");
+  std::string err;
+  if ((st = m->tab.check_prefill(n, slots, seq_lens, stop_lens, &err)) != SPR_OK) return fail(st, err);
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) total += seq_lens[i];
+  for (int64_t t = 0; t < total; ++t)
+    if (tokens[t] < 0 || tokens[t] >= m->d.V) return fail(SPR_ERR_INVALID_ARG, "prefill: token id out of range");
+
+  m->tab.commit_prefill(n, slots, seq_lens, stop_lens, retired);
+  Ptrs p{m->ws, &m->lay};
+  std::vector<int32_t> rows(static_cast<size_t>(n) * m->d.mb);
+  for (int i = 0; i < n; ++i) m->tab.block_row(slots[i], rows.data() + static_cast<size_t>(i) * m->d.mb);
+  for (int i = 0; i < n; ++i)
+    SPR_HIP(m, hipMemcpyAsync(p.bt() + static_cast<size_t>(slots[i]) * m->d.mb,
+                              rows.data() + static_cast<size_t>(i) * m->d.mb, m->d.mb * sizeof(int32_t),
+                              hipMemcpyHostToDevice, m->st));
+  SPR_HIP(m, hipStreamSynchronize(m->st));
+
+  RowSet rs;
+  rs.n = 0;
+  auto flush = [&](bool any_emit) -> spr_status {
+    if (rs.n == 0) return SPR_OK;
+    for (int r = rs.n; r < kRows; ++r) {
+      rs.slot[r] = 0;
+      rs.pos[r] = 0;
+      rs.out_row[r] = -1;
+      rs.tok[r] = 0;
+    }
+    spr_status s2 = forward_any(m, rs, nullptr, tok, logits, any_emit);
+    rs.n = 0;
+    return s2;
+  };
+  int64_t t = 0;
+  bool any_emit = false;
+  for (int i = 0; i < n; ++i) {
+    for (int pos = 0; pos < seq_lens[i]; ++pos, ++t) {
+      const int r = rs.n++;
+      rs.slot[r] = slots[i];
+      rs.pos[r] = pos;
+      rs.tok[r] = tokens[t];
+      rs.out_row[r] = pos == seq_lens[i] - 1 ? i : -1;
+      any_emit |= rs.out_row[r] >= 0;
+      if (rs.n == kRows) {
+        if ((st = flush(any_emit)) != SPR_OK) return st;
+        any_emit = false;
+      }
+    }
+  }
+  if ((st = flush(any_emit)) != SPR_OK) return st;
+  return SPR_OK;
+}
+
+spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots, const int32_t* lens, int32_t* tok,
+                           float* logits, int32_t* retired) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (slots == nullptr || lens == nullptr || tok == nullptr)
+    return fail(SPR_ERR_INVALID_ARG, "decode_step: slots, lens and tok must not be null");
+  std::string err;
+  if ((st = m->tab.check_decode(n_active, slots, lens, &err)) != SPR_OK) return fail(st, err);
+  RowSet rs;
+  rs.n = n_active;
+  for (int r = 0; r < kRows; ++r) {
+    const bool v = r < n_active;
+    rs.slot[r] = v ? slots[r] : 0;
+    rs.pos[r] = v ? lens[r] : 0;
+    rs.out_row[r] = v ? r : -1;
+    rs.tok[r] = 0;
+  }
+  if ((st = forward_any(m, rs, tok, tok, logits, true)) != SPR_OK) return st;
+  m->tab.commit_decode(n_active, slots, retired);
+  return SPR_OK;
+}
+
+spr_status spr_rewind_slot(spr_model* m, int32_t slot, int32_t len, int32_t produced) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  std::string err;
+  if ((st = m->tab.check_rewind(slot, len, produced, &err)) != SPR_OK) return fail(st, err);
+  m->tab.commit_rewind(slot, len, produced);
+  return SPR_OK;
+}
+
+spr_status spr_free_slot(spr_model* m, int32_t slot) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  std::string err;
+  if ((st = m->tab.check_free(slot, &err)) != SPR_OK) return fail(st, err);
+  m->tab.commit_free(slot);
+  return SPR_OK;
+}
+
+spr_status spr_slot_info(const spr_model* m, int32_t slot, int32_t* len, int32_t* produced, int32_t* stop_len) {
+  if (m == nullptr || len == nullptr || produced == nullptr || stop_len == nullptr)
+    return fail(SPR_ERR_INVALID_ARG, "slot_info: null argument");
+  if (slot < 0 || slot >= m->d.S) return fail(SPR_ERR_INVALID_ARG, "slot_info: slot id out of range");
+  const spr::Slot& s = m->tab.slot(slot);
+  *len = s.state == spr::kFree ? -1 : s.len;
+  *produced = s.produced;
+  *stop_len = s.stop;
+  return SPR_OK;
+}
+
+int32_t spr_free_blocks(const spr_model* m) { return m == nullptr ? -1 : m->tab.free_blocks(); }
+
+spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, int32_t row0, int32_t nrows,
+                                  float* out) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  const spr::Dims& d = m->d;
+  if (out == nullptr) return fail(SPR_ERR_INVALID_ARG, "export: out must not be null");
+  if (tensor < 0 || tensor > 8) return fail(SPR_ERR_INVALID_ARG, "export: tensor id must be in [0, 8]");
+  const bool per_layer = tensor >= 1 && tensor <= 7;
+  if (per_layer ? (layer < 0 || layer >= d.L) : layer != 0) return fail(SPR_ERR_INVALID_ARG, "export: bad layer");
+  static const int kind_of[9] = {-1, MK_QKV, MK_QKV, MK_QKV, MK_O, MK_W13, MK_W13, MK_W2, MK_LM};
+  static const int which_of[9] = {0, 0, 1, 2, 0, 0, 1, 0, 0};
+  int rows_total, cols;
+  switch (tensor) {
+    case 0: case 8: rows_total = d.V; cols = d.d; break;
+    case 1: rows_total = d.H * d.hd; cols = d.d; break;
+    case 2: case 3: rows_total = d.Hkv * d.hd; cols = d.d; break;
+    case 4: rows_total = d.d; cols = d.o_in; break;
+    case 5: case 6: rows_total = d.f; cols = d.d; break;
+    default: rows_total = d.d; cols = d.f;
+  }
+  if (row0 < 0 || nrows < 1 || static_cast<int64_t>(row0) + nrows > rows_total)
+    return fail(SPR_ERR_INVALID_ARG, "export: row range outside the matrix");
+  Ptrs p{m->ws, &m->lay};
+  const int64_t count = static_cast<int64_t>(nrows) * cols;
+  const bool bf = d.dtype == SPR_BF16;
+  if (tensor == 0) {
+    if (bf)
+      k_export_rowmajor<BF16><<<grid1(count), 256, 0, m->st>>>(reinterpret_cast<const uint16_t*>(p.emb()), cols,
+                                                               row0, nrows, out);
+    else
+      k_export_rowmajor<F32><<<grid1(count), 256, 0, m->st>>>(reinterpret_cast<const float*>(p.emb()), cols, row0,
+                                                              nrows, out);
+  } else {
+    const MatSpec s = mat_spec(d, kind_of[tensor], per_layer ? layer : 0, m->seed);
+    const char* base = tensor <= 3 ? p.wqkv(layer) : tensor == 4 ? p.wo(layer) : tensor <= 6 ? p.w13(layer)
+                                                   : tensor == 7 ? p.w2(layer) : p.wlm();
+    if (bf)
+      k_export_tiled<BF16><<<grid1(count), 256, 0, m->st>>>(reinterpret_cast<const uint16_t*>(base), s,
+                                                            which_of[tensor], row0, nrows, out);
+    else
+      k_export_tiled<F32><<<grid1(count), 256, 0, m->st>>>(reinterpret_cast<const float*>(base), s,
+                                                           which_of[tensor], row0, nrows, out);
+  }
+  SPR_LAUNCHED(m, "export");
+  return SPR_OK;
+}
+
+spr_status spr_release(spr_model* m) {
+  if (m == nullptr) return fail(SPR_ERR_INVALID_ARG, "release: model is null");
+  delete m;
+  return SPR_OK;
+}
+
+const char* spr_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

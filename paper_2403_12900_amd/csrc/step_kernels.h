@@ -1,0 +1,73 @@
+// Per-step kernels around the layer stack: token embedding and the final
+// greedy token (lowest index among equal maxima).
+#pragma once
+
+#include "gemm_kernels.h"
+
+namespace sprk {
+
+struct EmbedArgs {
+  const void* emb;          // [V][d] row-major
+  const int32_t* tok_dev;   // device tokens indexed by slot, or null: use tok[]
+  float* x;                 // residual [rows][d]
+  void* act;                // first activation, K-block-major over d
+  int n_rows, d, V, Rp;
+  int slot[kRows];
+  int tok[kRows];
+};
+
+// Tokens outside [0, V) (only possible when a caller forces them through
+// device memory) are clamped into range so no read leaves the table.
+template <class P>
+__global__ __launch_bounds__(64) void k_embed(EmbedArgs a) {
+  const int b = blockIdx.y;
+  const int n0 = 4 * (blockIdx.x * 64 + threadIdx.x);
+  if (n0 >= a.d) return;
+  int t = a.tok_dev != nullptr ? a.tok_dev[a.slot[b]] : a.tok[b];
+  t = min(max(t, 0), a.V - 1);
+  const typename P::elem* e = static_cast<const typename P::elem*>(a.emb) + static_cast<size_t>(t) * a.d + n0;
+  const float v0 = P::to_f32(e[0]), v1 = P::to_f32(e[1]), v2 = P::to_f32(e[2]), v3 = P::to_f32(e[3]);
+  *reinterpret_cast<float4*>(a.x + static_cast<size_t>(b) * a.d + n0) = make_float4(v0, v1, v2, v3);
+  store_act4<P>(static_cast<typename P::elem*>(a.act), a.Rp, b, n0, v0, v1, v2, v3);
+}
+
+struct ArgmaxArgs {
+  const float2* part;       // [tiles][kRows] (value, index bits)
+  int32_t* tok_dev;         // written at the row's slot
+  int n_tiles;
+  int slot[kRows];
+  int out_row[kRows];       // -1: row emits no token
+};
+
+__device__ __forceinline__ void better_of(float& v, int& i, float ov, int oi) {
+  if (ov > v || (ov == v && oi < i)) {
+    v = ov;
+    i = oi;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_argmax_final(ArgmaxArgs a) {
+  const int b = blockIdx.x;
+  if (a.out_row[b] < 0) return;
+  float v = -INFINITY;
+  int idx = 0x7fffffff;
+  for (int t = threadIdx.x; t < a.n_tiles; t += 256) {
+    const float2 p = a.part[static_cast<size_t>(t) * kRows + b];
+    better_of(v, idx, p.x, __float_as_int(p.y));
+  }
+  for (int o = 32; o >= 1; o >>= 1) better_of(v, idx, __shfl_xor(v, o), __shfl_xor(idx, o));
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    sv[wave] = v;
+    si[wave] = idx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) better_of(v, idx, sv[w], si[w]);
+    a.tok_dev[a.slot[b]] = idx;
+  }
+}
+
+}  // namespace sprk

@@ -1,0 +1,226 @@
+"""Device decode vs the CPU oracle, through the C ABI (needs an MI355X).
+
+Every case runs the device free-running (greedy) and feeds the device's own
+tokens to the oracle (teacher forcing), so both see the same inputs at every
+step.  Gates per (request, step) logits row:
+  * fp32 models: max abs error <= 1e-4 and relative L2 <= 1e-5;
+  * bf16 models: max abs error <= 5e-2 and relative L2 <= 1e-2;
+  * greedy tokens: the argmax of the device's own logits exactly, and the
+    oracle's argmax unless the oracle's top-2 margin is within 2 max|dz|;
+  * retirement bookkeeping: bit-exact against the closed form.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+from oracle import _clib
+from oracle import llama_ref as R
+from paper_2403_12900_amd.configs import CONFIGS, LLAMA2_7B, ModelConfig
+from paper_2403_12900_amd.workload import make_workload
+
+from ._harness import DeviceRun, check_against_oracle, oracle_shape, say
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = (1e-4, 1e-5)
+BF16_TOL = (5e-2, 1e-2)
+
+
+def _tol(m: ModelConfig):
+    return BF16_TOL if m.bf16 else FP32_TOL
+
+
+def _prompts(rng, V, lens):
+    return [rng.integers(0, V, size=n).astype(np.int32) for n in lens]
+
+
+# ------------------------------------------------------------------ weights
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_weight_generator_bit_exact(bf16):
+    m = ModelConfig(n_layers=2, d_model=48, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=40, vocab=70, bf16=bf16)
+    say(f"weights bit-exact bf16={bf16}")
+    from paper_2403_12900_amd.binding import DecodeModel
+    dm = DecodeModel(m, seed=424242, max_slots=2, max_ctx=32)
+    sh = oracle_shape(m)
+    for name in ("embed", "wq", "wk", "wv", "wo", "w1", "w3", "w2", "lm_head"):
+        rows, cols = sh.matrix_dims(name)
+        for layer in ((0, 1) if name not in ("embed", "lm_head") else (0,)):
+            got = dm.export_weight_rows(name, layer, 0, rows, cols).cpu().numpy()
+            want = _clib.wgen_rows(424242, R.TENSOR_IDS[name], layer, cols, 0, rows, bf16, dtype=np.float32)
+            assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), (name, layer)
+    dm.close()
+
+
+def test_weight_generator_bit_exact_7b_rows():
+    """Sampled rows of every Llama-2-7B matrix, including the fused QKV and interleaved gate/up layouts."""
+    say("weights bit-exact 7B sampled rows")
+    from paper_2403_12900_amd.binding import DecodeModel
+    m = LLAMA2_7B
+    dm = DecodeModel(m, seed=1003, max_slots=1, max_ctx=16)
+    sh = oracle_shape(m)
+    for name in ("embed", "wq", "wk", "wv", "wo", "w1", "w3", "w2", "lm_head"):
+        rows, cols = sh.matrix_dims(name)
+        layers = (0,) if name in ("embed", "lm_head") else (0, 31)
+        for layer in layers:
+            for r0 in (0, rows // 2 + 3, rows - 2):
+                got = dm.export_weight_rows(name, layer, r0, 2, cols).cpu().numpy()
+                want = _clib.wgen_rows(1003, R.TENSOR_IDS[name], layer, cols, r0, 2, True, dtype=np.float32)
+                assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), (name, layer, r0)
+    dm.close()
+
+
+# ------------------------------------------------------------------ tiny configuration (fp32)
+
+def test_tiny_config_all_steps():
+    """The tiny fp32 configuration end to end: every request, every step."""
+    cfg = CONFIGS["c1"]
+    wl = make_workload(cfg)
+    say("tiny config c1")
+    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, wl.stop_lens.tolist())
+    assert run.active == R.active_schedule(wl.stop_lens.tolist())
+    assert [len(t) for t in run.tokens] == wl.stop_lens.tolist()
+    w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed)
+    st = check_against_oracle(run, w, wl.tokens, wl.stop_lens, range(wl.batch), *FP32_TOL)
+    say("c1", st)
+    assert st["rows"] == int(wl.stop_lens.sum())
+    run.close()
+
+
+# ------------------------------------------------------------------ toy shapes: tails and paths
+
+TOY_CASES = {
+    # name: (model, prompt lengths, stop lengths)
+    "bf16_mha_hd64_ragged": (
+        ModelConfig(n_layers=2, d_model=128, n_heads=2, n_kv_heads=2, head_dim=64, d_ff=200, vocab=1000),
+        [15, 16, 17, 1, 31, 32, 33, 47], [3, 5, 2, 9, 1, 4, 6, 2]),
+    "bf16_gqa4_hd128_wide_o": (
+        ModelConfig(n_layers=2, d_model=256, n_heads=8, n_kv_heads=2, head_dim=128, d_ff=344, vocab=777),
+        [5, 64, 100, 3, 18, 77, 19, 2, 40, 9, 12, 33, 1, 60, 8, 16, 17, 90, 4, 25], [4] * 10 + [2, 7] * 5),
+    "fp32_gqa2_hd128": (
+        ModelConfig(n_layers=1, d_model=64, n_heads=2, n_kv_heads=1, head_dim=128, d_ff=100, vocab=50,
+                    bf16=False),
+        [3, 20, 16, 1, 45], [6, 2, 3, 4, 5]),
+    "bf16_batch40_jt4": (
+        ModelConfig(n_layers=1, d_model=64, n_heads=1, n_kv_heads=1, head_dim=64, d_ff=64, vocab=300),
+        list(range(1, 41)), [3] * 40),
+    "bf16_long_context_splits": (
+        ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=128, vocab=500),
+        [700, 300], [20, 3]),
+}
+
+
+@pytest.mark.parametrize("case", sorted(TOY_CASES))
+def test_toy_shapes(case):
+    m, plens, stops = TOY_CASES[case]
+    say(f"toy {case}")
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
+    prompts = _prompts(rng, m.vocab, plens)
+    run = DeviceRun(m, 77, prompts, stops)
+    assert run.active == R.active_schedule(stops)
+    w = R.Weights(oracle_shape(m), 77)
+    st = check_against_oracle(run, w, prompts, stops, range(len(prompts)), *_tol(m))
+    say(case, st)
+    run.close()
+
+
+def test_forced_tokens_and_in_place_buffer():
+    """Teacher forcing through the device token buffer equals the oracle fed the same tokens."""
+    m, plens, stops = TOY_CASES["bf16_mha_hd64_ragged"]
+    say("forced tokens")
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    rng = np.random.default_rng(5)
+    prompts = _prompts(rng, m.vocab, [9, 20])
+    dm = DecodeModel(m, 78, max_slots=2, max_ctx=64)
+    tok = dm.new_token_buffer()
+    dm.prefill([0, 1], prompts, [5, 5], tok)
+    forced = rng.integers(0, m.vocab, size=(4, 2)).astype(np.int32)
+    lens = [9, 20]
+    got = []
+    for s in range(4):
+        tok.copy_(torch.from_numpy(forced[s]).to(tok.device))
+        lg, _ = dm.decode_step([0, 1], lens, tok, want_logits=True)
+        got.append(lg.cpu().numpy())
+        lens = [l + 1 for l in lens]
+    w = R.Weights(oracle_shape(m), 78)
+    for i in range(2):
+        ref = R.forward_causal(w, list(prompts[i]) + forced[:, i].tolist(),
+                               [len(prompts[i]) + s for s in range(4)])
+        for s in range(4):
+            d = np.abs(got[s][i] - ref[s]).max()
+            assert d <= BF16_TOL[0], (i, s, d)
+    dm.close()
+
+
+def test_rewind_regenerates_identically():
+    m, _, _ = TOY_CASES["bf16_gqa4_hd128_wide_o"]
+    say("rewind")
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    rng = np.random.default_rng(6)
+    prompts = _prompts(rng, m.vocab, [30, 7])
+    dm = DecodeModel(m, 79, max_slots=2, max_ctx=64)
+    tok = dm.new_token_buffer()
+    dm.prefill([0, 1], prompts, [6, 6], tok)
+    first = tok.clone()
+
+    def run():
+        out = []
+        lens = [30, 7]
+        for _ in range(5):
+            dm.decode_step([0, 1], lens, tok)
+            out.append(tok.cpu().numpy().copy())
+            lens = [l + 1 for l in lens]
+        return np.stack(out)
+
+    a = run()
+    dm.rewind(0, 30, 1)
+    dm.rewind(1, 7, 1)
+    tok.copy_(first)
+    b = run()
+    assert np.array_equal(a, b)
+    dm.close()
+
+
+def test_batch_invariance():
+    """A request decoded alone or inside a batch gives the same tokens and logits within tolerance."""
+    m, plens, stops = TOY_CASES["bf16_gqa4_hd128_wide_o"]
+    say("batch invariance")
+    rng = np.random.default_rng(7)
+    prompts = _prompts(rng, m.vocab, plens)
+    full = DeviceRun(m, 80, prompts, stops)
+    for i in (1, 13):
+        alone = DeviceRun(m, 80, [prompts[i]], [stops[i]])
+        for s, z in alone.logits[0].items():
+            assert np.abs(z - full.logits[i][s]).max() <= BF16_TOL[0]
+        alone.close()
+    full.close()
+
+
+# ------------------------------------------------------------------ Llama-2-7B shape, ragged batch 32
+
+def test_llama2_7b_ragged_batch32_sampled():
+    """The benchmarked workload at full size: all 32 requests decode to their
+    stop lengths; the oracle checks the two shortest requests at every step it
+    can afford (prefill, early, middle and final steps)."""
+    cfg = CONFIGS["c3"]
+    wl = make_workload(cfg)
+    seq, stops = wl.seq_lens, wl.stop_lens
+    order = np.argsort(seq + stops)
+    sampled = [int(order[0]), int(order[1])]
+    steps = {}
+    for i in sampled:
+        L = int(stops[i])
+        steps[i] = sorted({0, 1, 2, L // 2, L - 2, L - 1} & set(range(L)))
+    record = set().union(*steps.values())
+    say(f"7B ragged batch 32: sampled requests {sampled}, steps {steps}")
+    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops.tolist(), record=record)
+    assert run.active == R.active_schedule(stops.tolist())
+    assert [len(t) for t in run.tokens] == stops.tolist()
+    w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed, resident=False)
+    st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL, steps_of=lambda i: steps[i])
+    say("c3 sampled", st)
+    assert st["rows"] == sum(len(v) for v in steps.values())
+    run.close()

@@ -7,6 +7,7 @@ they are chosen so that a dropped term, a wrong sign or index, or a
 transposed operand anywhere in oracle/llama_ref.py or oracle/wgen.c fails at
 least one of them.
 """
+import dataclasses
 import math
 import os
 
@@ -21,6 +22,9 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 TOY = R.Shape(n_layers=2, d_model=32, n_heads=4, n_kv_heads=2, head_dim=8, d_ff=40, vocab=50, bf16=True)
 TOY_MHA = R.Shape(n_layers=1, d_model=16, n_heads=2, n_kv_heads=2, head_dim=8, d_ff=24, vocab=20, bf16=False)
+# The brute-force forward below keeps cached keys/values exact.
+TOY_EXACT_KV = dataclasses.replace(TOY, kv_round=False)
+TOY_MHA_EXACT_KV = dataclasses.replace(TOY_MHA, kv_round=False)
 
 
 # ---------------------------------------------------------------- generator
@@ -288,13 +292,41 @@ def _py_forward_toy(w: R.Weights, tokens):
     return np.array([mv(lm, norm(x)) for x in xs])
 
 
-@pytest.mark.parametrize("shape", [TOY, TOY_MHA], ids=["gqa_bf16", "mha_fp32"])
+@pytest.mark.parametrize("shape", [TOY_EXACT_KV, TOY_MHA_EXACT_KV], ids=["gqa_bf16", "mha_fp32"])
 def test_forward_matches_brute_force(shape):
     w = R.Weights(shape, seed=11)
     toks = [3, 17, 0, shape.vocab - 1, 8, 8]
     got = R.forward_causal(w, toks)
     ref = _py_forward_toy(w, toks)
     assert np.allclose(got, ref, rtol=1e-10, atol=1e-12)
+
+
+def test_round_to_storage():
+    # Near 1 the bf16 grid spacing is 2^-7.  1 + 2^-8 is a tie and goes to the
+    # even neighbour 1.0; 1 + 3 * 2^-8 is a tie between 1 + 2^-7 (odd) and
+    # 1 + 2^-6 (even) and goes to 1 + 2^-6.
+    x = np.array([1.0, 1 + 2**-8, 1 + 3 * 2**-8, -2.5, 1e-3, 0.0])
+    b = R.round_to_storage(x, True)
+    assert b.tolist()[:4] == [1.0, 1.0, 1 + 2**-6, -2.5]
+    assert np.all((b.astype(np.float32).view(np.uint32) & 0xFFFF) == 0)
+    assert abs(b[4] - 1e-3) <= 1e-3 * 2**-8
+    f = R.round_to_storage(np.array([1 + 2**-30]), False)
+    assert f[0] == 1.0                      # fp32 rounding
+
+
+def test_kv_cache_storage_rounding_is_small_and_consistent():
+    """Rounded and exact caches give close logits; incremental == recompute holds for both."""
+    w_r = R.Weights(TOY, seed=21)
+    w_e = R.Weights(TOY_EXACT_KV, seed=21)
+    toks = [3, 9, 27, 4, 4, 11, 2]
+    a = R.forward_causal(w_r, toks)
+    b = R.forward_causal(w_e, toks)
+    assert 0 < np.abs(a - b).max() < 1e-2 * np.abs(b).max()
+    # The cache the incremental decoder holds is on the bf16 grid.
+    dec = R.KVCacheDecoder(w_r)
+    dec.prefill(0, toks, capacity=len(toks))
+    K = dec.K[0][1][: len(toks)]
+    assert np.all((K.astype(np.float32).view(np.uint32) & 0xFFFF) == 0)
 
 
 def test_layer_streaming_matches_resident():
