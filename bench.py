@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Decode throughput of the benchmarked workload on one MI355X.
+
+Workload (synthetic, seeded): Llama-2-7B shape, bf16 weights and KV cache,
+a closed batch of 32 requests with lognormal prompt lengths (median 200), a
+directive level per request (prefix 0 / 8 / 12 tokens) and lognormal
+generation lengths by level (medians 400 / 120 / 40); each request retires at
+its own stop length.  One bench step is one full ragged decode of that batch
+-- every decode step from the prefilled cache until the last request retires
+-- so a step's tokens are sum(L_i - 1).  Inputs (weights, KV cache, first
+tokens) are resident in HBM when the timed region starts; prefill is outside
+it.
+
+Prints one JSON line on stdout (progress goes to stderr).
+"""
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/s + achieved HBM GB/s, Llama-2-7B-shape bf16, ragged batch 32"
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
+DOMINANT = "k_stream_gemm<BF16, 1, 4, EpiSwiGLU<BF16>, 1, 8, true>"
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_gemm_pmc_llama2_7b_b8.txt")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2403_12900_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(bytes_per_launch: float):
+    """HBM bytes per launch of the dominant kernel from the committed PMC summary,
+    or None when the kernel sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_PROFILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, wl, seconds: float):
+    """The CPU oracle's KV-cache decode step on the same workload, bounded sample."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import llama_ref as R
+    m = cfg.model
+    sh = R.Shape(m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff, m.vocab,
+                 m.rope_base, m.rms_eps, m.bf16)
+    t0 = time.perf_counter()
+    w = R.Weights(sh, cfg.weight_seed, resident=True)
+    for l in range(sh.n_layers):
+        w.layer(l)
+    w.matrix("embed")
+    w.matrix("lm_head")
+    log(f"cpu baseline: oracle weights drawn in {time.perf_counter() - t0:.1f} s")
+    dec = R.KVCacheDecoder(w)
+    B = wl.batch
+    max_steps = 64
+    seq = wl.seq_lens
+    for i in range(B):
+        dec.attach_cache(i, int(seq[i]) + max_steps + 1, int(seq[i]))
+    tok = [int(t[-1]) for t in wl.tokens]
+    done = steps = 0
+    t0 = time.perf_counter()
+    while steps < max_steps and time.perf_counter() - t0 < seconds:
+        active = [i for i in range(B) if wl.stop_lens[i] > steps + 1]
+        z = dec.step(active, [tok[i] for i in active])
+        for k, i in enumerate(active):
+            tok[i] = int(np.argmax(z[k]))
+        done += len(active)
+        steps += 1
+    el = time.perf_counter() - t0
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    cores = max((p.get("num_threads", 1) for p in blas), default=1)
+    return {"value": done / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {steps} decode steps of the same batch ({done} tokens, {el:.1f} s), fp64 numpy "
+                      f"KV-cache decode with resident weights; caches sized to the real prompts, prefill not run"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}): the decode path runs one model "
+              "replica per GPU with no exchange between GPUs, and this build has no multi-GPU mode.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    from paper_2403_12900_amd.workload import make_workload, workload_stats
+
+    cfg = CONFIGS["c3"]
+    m = cfg.model
+    wl = make_workload(cfg)
+    st = workload_stats(cfg, wl)
+    B = wl.batch
+    seq = [int(x) for x in wl.seq_lens]
+    stops = [int(x) for x in wl.stop_lens]
+    max_ctx = max(s + L - 1 for s, L in zip(seq, stops))
+    blocks = sum((s + L - 1 + 15) // 16 for s, L in zip(seq, stops))
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    model = DecodeModel(m, cfg.weight_seed, max_slots=B, max_ctx=max_ctx, kv_blocks=blocks)
+    tok = model.new_token_buffer()
+    model.prefill(list(range(B)), wl.tokens, stops, tok)
+    tok0 = tok.clone()
+    torch.cuda.synchronize()
+    log(f"init + prefill {time.perf_counter() - t0:.1f} s; {st['steps']} decode steps, "
+        f"{st['decode_tokens']} tokens, avg active {st['avg_active']:.2f}")
+
+    schedule = []
+    for s in range(1, max(stops)):
+        act = [i for i in range(B) if stops[i] > s]
+        schedule.append((act, [seq[i] + s - 1 for i in act]))
+
+    def one_step():
+        for i in range(B):
+            if stops[i] > 1:
+                model.rewind(i, seq[i], 1)
+        tok.copy_(tok0)
+        for act, lens in schedule:
+            model.decode_step(act, lens, tok)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        one_step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / args.steps
+    tokens = st["decode_tokens"]
+    value = tokens / (ms / 1e3)
+    gbps = st["bytes"] / (ms / 1e3) / 1e9
+    log(f"decode: {ms:.1f} ms per ragged batch (wall {1e3 * wall / args.steps:.1f} ms), {value:.0f} tokens/s, "
+        f"{gbps:.0f} GB/s algorithmic")
+
+    # Dominant kernel: the gate/up projection with SwiGLU (largest weight stream of a layer).
+    n_probe = 8
+    reps = 200
+    us = model.time_projection("gate_up", n_probe, reps)
+    elem = 2 * m.d_ff * m.d_model
+    per_launch = elem * 2 + n_probe * m.d_model * 2 * 2 + n_probe * m.d_ff * 2 * 2
+    achieved = per_launch / (us * 1e-6) / 1e9
+    others = {}
+    for name, el in (("o", m.d_model * m.n_heads * m.head_dim), ("down", m.d_model * m.d_ff),
+                     ("lm_head", m.vocab * m.d_model)):
+        u = model.time_projection(name, n_probe, 50)
+        others[name] = {"us": round(u, 2), "gbps": round(el * 2 / (u * 1e-6) / 1e9, 1)}
+    traffic = measured_traffic(per_launch)
+    log(f"gate/up kernel: {us:.2f} us per launch, {achieved:.0f} GB/s; others {others}")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "achieved_hbm_gbps": round(gbps, 1),
+        "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+        "config": {"workload": cfg.name, "batch": B, "decode_steps": st["steps"],
+                   "decode_tokens_per_step": tokens, "avg_active": round(st["avg_active"], 3),
+                   "algorithmic_bytes_per_step": st["bytes"], "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": DOMINANT, "rows": n_probe, "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": traffic, "bytes_per_launch": per_launch, "us_per_launch": round(us, 3),
+                     "other_projections": others},
+    }
+    model.close()
+    del model
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_seconds)
+        log(f"cpu baseline: {out['cpu_baseline']}")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -161,6 +161,21 @@ int32_t spr_free_blocks(const spr_model* m);
 spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, int32_t row0, int32_t nrows,
                                   float* out);
 
+/*
+ * Measurement aid: enqueues `reps` back-to-back launches of one projection
+ * kernel exactly as a decode step over n_rows rows launches it (launch r uses
+ * layer r mod n_layers, so every layer's weights are streamed in turn),
+ * brackets them with HIP events on the model's stream, waits, and writes the
+ * mean launch duration in microseconds to *avg_us.  projection: 1 = O
+ * (x += o Wo^T), 2 = gate/up with SwiGLU, 3 = down (x += h W2^T), 4 = LM head
+ * with the greedy candidates.  It reads and writes only the forward pass's
+ * scratch buffers (activations, residual, greedy candidates), which every
+ * decode step rewrites before reading, so cached state is untouched; the QKV
+ * projection, which appends to the KV cache, is refused (SPR_ERR_INVALID_ARG).
+ * n_rows 1..128, reps 1..100000.  Synchronous.
+ */
+spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
+
 /* Releases the host state.  The workspace is the caller's to free afterwards. */
 spr_status spr_release(spr_model* m);
 

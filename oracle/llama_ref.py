@@ -352,6 +352,15 @@ class KVCacheDecoder:
         sh = self.w.shape
         return rmsnorm(x, self.w.gain(), sh.rms_eps) @ self.w.matrix("lm_head").T
 
+    def attach_cache(self, rid: int, capacity: int, length: int):
+        """A request whose first `length` positions count as cached (zero-valued).
+
+        Only for timing decode steps: the work of a step depends on the cache
+        sizes, not on the cached values, so the prefill can be skipped.
+        """
+        self._alloc(rid, capacity)
+        self.len[rid] = length
+
     def prefill(self, rid: int, tokens: Sequence[int], capacity: int) -> np.ndarray:
         """Fills the cache with the prompt (directive prefix first) and returns the logits of its last position."""
         self._alloc(rid, capacity)

@@ -68,6 +68,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_free_blocks.argtypes = [vp]
     L.spr_export_weight_rows.restype = ctypes.c_int
     L.spr_export_weight_rows.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp]
+    L.spr_time_projection.restype = ctypes.c_int
+    L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.POINTER(ctypes.c_float)]
     L.spr_release.restype = ctypes.c_int
     L.spr_release.argtypes = [vp]
     L.spr_last_error.restype = ctypes.c_char_p
@@ -171,6 +174,14 @@ class DecodeModel:
         _check(self.lib.spr_export_weight_rows(self.h, TENSOR_IDS[tensor], layer, row0, nrows,
                                                ctypes.c_void_p(out.data_ptr())))
         return out
+
+    PROJECTIONS = {"o": 1, "gate_up": 2, "down": 3, "lm_head": 4}
+
+    def time_projection(self, projection: str, n_rows: int, reps: int) -> float:
+        """Mean launch duration (us) of one projection kernel, timed with HIP events on the model's stream."""
+        out = ctypes.c_float()
+        _check(self.lib.spr_time_projection(self.h, self.PROJECTIONS[projection], n_rows, reps, ctypes.byref(out)))
+        return float(out.value)
 
     def close(self):
         if getattr(self, "h", None) is not None and self.h.value:

@@ -25,7 +25,7 @@ namespace sprk {
 
 struct AttnArgs {
   const float* q;         // [rows][H][hd], fp32
-  const void* kc;         // this layer's K blocks [block][Hkv][16][hd]
+  const void* kc;         // this layer's K blocks [block][Hkv][16 x hd in fragment order]
   const void* vc;         // this layer's V blocks [block][Hkv][hd][16]
   const int32_t* bt;      // [slots][mb]
   void* act;              // output, K-block-major over H * hd
@@ -46,25 +46,27 @@ struct VQuad;
 template <>
 struct VQuad<BF16> {
   uint2 raw;
-  __device__ __forceinline__ void load(const uint16_t* v) { raw = *reinterpret_cast<const uint2*>(v); }
+  __device__ __forceinline__ void load(const uint16_t* v) {
+    typedef unsigned int u2v __attribute__((ext_vector_type(2)));
+    const u2v t = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(v));
+    raw = make_uint2(t.x, t.y);
+  }
   // Positions past the context hold stale or never-written cache memory; they
   // get probability 0, but 0 * NaN would still poison the sum, so zero them.
   __device__ __forceinline__ void mask(int valid) {
-    if (valid <= 0) raw.x = 0u;
-    else if (valid == 1) raw.x &= 0xFFFFu;
-    if (valid <= 2) raw.y = 0u;
-    else if (valid == 3) raw.y &= 0xFFFFu;
+    raw.x &= valid >= 2 ? 0xFFFFFFFFu : valid == 1 ? 0xFFFFu : 0u;
+    raw.y &= valid >= 4 ? 0xFFFFFFFFu : valid == 3 ? 0xFFFFu : 0u;
   }
 };
 template <>
 struct VQuad<F32> {
   uint4 raw;
-  __device__ __forceinline__ void load(const float* v) { raw = *reinterpret_cast<const uint4*>(v); }
+  __device__ __forceinline__ void load(const float* v) { raw = load_weight<true>(reinterpret_cast<const uint4*>(v)); }
   __device__ __forceinline__ void mask(int valid) {
-    if (valid <= 0) raw.x = 0u;
-    if (valid <= 1) raw.y = 0u;
-    if (valid <= 2) raw.z = 0u;
-    if (valid <= 3) raw.w = 0u;
+    raw.x = valid >= 1 ? raw.x : 0u;
+    raw.y = valid >= 2 ? raw.y : 0u;
+    raw.z = valid >= 3 ? raw.z : 0u;
+    raw.w = valid >= 4 ? raw.w : 0u;
   }
 };
 
@@ -91,28 +93,61 @@ __device__ __forceinline__ f32x4_t mma_tok16(f32x4_t acc, const VQuad<F32>& v, c
   return acc;
 }
 
+// K and V of one 16-position block of one KV head, in registers.  Each cached
+// byte is read once per step, so the loads are streaming (nontemporal).
+template <class P, int HD>
+struct KVBlock {
+  using E = typename P::elem;
+  static constexpr int NF = HD / P::kblk;  // K fragments (1 KiB each)
+  static constexpr int NE = HD / 16;       // V^T fragments, 16 dims each
+  uint4 kf[NF];
+  VQuad<P> vq[NE];
+
+  __device__ __forceinline__ void load(const E* kc, const E* vc, size_t tile, int lane) {
+    const uint4* kt = reinterpret_cast<const uint4*>(kc + tile * 16 * HD) + lane;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) kf[f] = load_weight<true>(kt + f * 64);
+    const E* vt = vc + (tile * HD + (lane & 15)) * 16 + 4 * (lane >> 4);
+#pragma unroll
+    for (int e = 0; e < NE; ++e) vq[e].load(vt + e * 16 * 16);
+  }
+};
+
+// Work-group (split s, row b, KV head): blocks [s * bps, min(nblk, (s + 1) *
+// bps)); wave w takes the contiguous run of bps / 4 blocks starting at
+// w * bps / 4.  A wave walks its blocks one at a time -- load K and V, scores,
+// online-softmax update, P V -- with few registers, so that several waves per
+// SIMD hide each other's memory latency (measured faster on MI355X than
+// keeping two blocks in flight per wave at lower occupancy).  Branch
+// conditions are wave-uniform; the partial last block of the context is
+// masked by selects.
 template <class P, int HD>
 __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   using E = typename P::elem;
+  using Blk = KVBlock<P, HD>;
   constexpr bool kBf16 = sizeof(E) == 2;
-  constexpr int NF = HD * static_cast<int>(sizeof(E)) / 64;  // 16-byte fragments per lane per key row
-  constexpr int SEG = HD / 4;                                // dims per lane group
-  constexpr int NE = HD / 16;                                // 16-dim output chunks
+  constexpr int NF = Blk::NF;
+  constexpr int NE = Blk::NE;
   const int s = blockIdx.x, b = blockIdx.y, kvh = blockIdx.z;
   const int pos = a.rows.pos[b];
   const int ctx = pos + 1;
   const int nblk = (ctx + 15) >> 4;
   const int nsplit = (nblk + a.bps - 1) / a.bps;
   if (s >= nsplit) return;
-  const int lo = s * a.bps, hi = min(nblk, lo + a.bps);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane & 15, g = lane >> 4;
   const bool hv = h < a.G;
+  const int bpw = a.bps / 4;
+  const int lo = min(nblk, s * a.bps + wave * bpw), hi = min(nblk, s * a.bps + (wave + 1) * bpw);
+  const int32_t* btrow = a.bt + static_cast<size_t>(a.rows.slot[b]) * a.mb;
 
-  // Q^T operand (hi and lo parts for bf16), scaled so scores are in log2 units.
+  // Q^T operand (hi and lo parts for bf16), scaled so scores are in log2
+  // units; fragment c, lane h + 16 g holds dims c * kblk + g * per16 + j,
+  // matching the K tile order.
   uint4 qh[NF], ql[NF];
   {
-    const float* qp = a.q + (static_cast<size_t>(b) * a.H + kvh * a.G + (hv ? h : 0)) * HD + g * SEG;
+    const float* qp = a.q + (static_cast<size_t>(b) * a.H + kvh * a.G + (hv ? h : 0)) * HD + g * P::per16;
 #pragma unroll
     for (int c = 0; c < NF; ++c) {
       union {
@@ -121,7 +156,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
       } vh, vl;
 #pragma unroll
       for (int j = 0; j < P::per16; ++j) {
-        const float v = hv ? qp[c * P::per16 + j] * a.qscale : 0.f;
+        const float v = hv ? qp[c * P::kblk + j] * a.qscale : 0.f;
         vh.e[j] = P::from_f32(v);
         vl.e[j] = P::from_f32(v - P::to_f32(vh.e[j]));
       }
@@ -134,53 +169,43 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
 #pragma unroll
   for (int e = 0; e < NE; ++e) O[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const int32_t* btrow = a.bt + static_cast<size_t>(a.rows.slot[b]) * a.mb;
   const E* kc = static_cast<const E*>(a.kc);
   const E* vc = static_cast<const E*>(a.vc);
 
-  for (int i = lo + wave; i < hi; i += 4) {
-    const size_t tile = static_cast<size_t>(btrow[i]) * a.Hkv + kvh;
-    const uint4* kt = reinterpret_cast<const uint4*>(kc + (tile * 16 + (lane & 15)) * HD + g * SEG);
-    uint4 kf[NF];
-#pragma unroll
-    for (int c = 0; c < NF; ++c) kf[c] = kt[c];
-    const E* vt = vc + (tile * HD + (lane & 15)) * 16 + 4 * g;
-    VQuad<P> vq[NE];
-#pragma unroll
-    for (int e = 0; e < NE; ++e) vq[e].load(vt + e * 16 * 16);
-
+  for (int i = lo; i < hi; ++i) {
+    Blk B;
+    B.load(kc, vc, static_cast<size_t>(btrow[i]) * a.Hkv + kvh, lane);
     f32x4_t S = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NF; ++c) {
-      S = P::mma(S, kf[c], qh[c]);
-      if constexpr (kBf16) S = P::mma(S, kf[c], ql[c]);
+    for (int f = 0; f < NF; ++f) {
+      S = P::mma(S, B.kf[f], qh[f]);
+      if constexpr (kBf16) S = P::mma(S, B.kf[f], ql[f]);
     }
-    const int t0 = i * 16 + 4 * g;
-    if (t0 + 4 > ctx) {
+    if (i == nblk - 1) {  // the block holding the context's last position
+      const int valid = ctx - (i * 16 + 4 * g);
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (t0 + r >= ctx) S[r] = -INFINITY;
+      for (int r = 0; r < 4; ++r) S[r] = r < valid ? S[r] : -INFINITY;
 #pragma unroll
-      for (int e = 0; e < NE; ++e) vq[e].mask(ctx - t0);
+      for (int e = 0; e < NE; ++e) B.vq[e].mask(valid);
     }
     float mb = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
     mb = fmaxf(mb, __shfl_xor(mb, 16));
     mb = fmaxf(mb, __shfl_xor(mb, 32));
     const float m_new = fmaxf(m_run, mb);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     float p[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) p[r] = exp2f(S[r] - m_new);
+    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(S[r] - m_new);
     l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    m_run = m_new;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
       O[e][0] *= alpha;
       O[e][1] *= alpha;
       O[e][2] *= alpha;
       O[e][3] *= alpha;
-      O[e] = mma_tok16(O[e], vq[e], p);
+      O[e] = mma_tok16(O[e], B.vq[e], p);
     }
-    m_run = m_new;
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
@@ -196,16 +221,18 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   }
   __syncthreads();
   if (wave != 0) return;
+  // Wave 0 always holds at least one block (lo < nblk for s < nsplit), so M is
+  // finite; waves without blocks carry m = -inf and weigh 0.
   float M = m_run;
   for (int w = 0; w < 3; ++w) M = fmaxf(M, sm[w][0][lane]);
-  const float c0 = exp2f(m_run - M);
+  const float c0 = __builtin_amdgcn_exp2f(m_run - M);
   float L = l_run * c0;
 #pragma unroll
   for (int e = 0; e < NE; ++e)
 #pragma unroll
     for (int r = 0; r < 4; ++r) O[e][r] *= c0;
   for (int w = 0; w < 3; ++w) {
-    const float cw = exp2f(sm[w][0][lane] - M);
+    const float cw = __builtin_amdgcn_exp2f(sm[w][0][lane] - M);
     L += cw * sm[w][1][lane];
 #pragma unroll
     for (int e = 0; e < NE; ++e)
@@ -233,23 +260,34 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   }
 }
 
-// Log-sum-exp merge of the KV splits of rows that needed more than one.
+// Log-sum-exp merge of the KV splits of rows that needed more than one.  All
+// splits' statistics and values are loaded before any is combined.
 template <class P, int HD>
 __global__ __launch_bounds__(HD) void k_attn_merge(AttnArgs a) {
   const int b = blockIdx.x, hq = blockIdx.y, dd = threadIdx.x;
   const int nsplit = attn_nsplit(a.rows.pos[b], a.bps);
   if (nsplit <= 1) return;
   const float* pp = a.part + (static_cast<size_t>(b) * a.H + hq) * kSplitsMax * (HD + 4);
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pp[s * (HD + 4)]);
+  float m[kSplitsMax], l[kSplitsMax], o[kSplitsMax];
+#pragma unroll
+  for (int s = 0; s < kSplitsMax; ++s) {
+    const bool v = s < nsplit;
+    m[s] = v ? pp[s * (HD + 4)] : -INFINITY;
+    l[s] = v ? pp[s * (HD + 4) + 1] : 0.f;
+    o[s] = v ? pp[s * (HD + 4) + 4 + dd] : 0.f;
+  }
+  float M = m[0];
+#pragma unroll
+  for (int s = 1; s < kSplitsMax; ++s) M = fmaxf(M, m[s]);
   float L = 0.f, O = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float c = exp2f(pp[s * (HD + 4)] - M);
-    L += c * pp[s * (HD + 4) + 1];
-    O += c * pp[s * (HD + 4) + 4 + dd];
+#pragma unroll
+  for (int s = 0; s < kSplitsMax; ++s) {
+    const float c = __builtin_amdgcn_exp2f(m[s] - M);
+    L += c * l[s];
+    O += c * o[s];
   }
   const int k = hq * HD + dd;
-  P::store_act(act_record<P>(static_cast<typename P::elem*>(a.act), a.Rp, b, k), k % P::kblk, O / L);
+  act_store<P>(static_cast<typename P::elem*>(a.act), a.Rp, b, k, O / L);
 }
 
 }  // namespace sprk

@@ -56,11 +56,10 @@ struct BF16 {
     }
     return s;
   }
-  // Writes activation value v at element kk of the (K-block, row) record `rec`.
-  static __device__ __forceinline__ void store_act(elem* rec, int kk, float v) {
-    const elem hi = from_f32(v);
-    rec[kk] = hi;
-    rec[kblk + kk] = from_f32(v - to_f32(hi));
+  // The hi and lo parts of an activation value.
+  static __device__ __forceinline__ void split(float v, elem* hi, elem* lo) {
+    *hi = from_f32(v);
+    *lo = from_f32(v - to_f32(*hi));
   }
 };
 
@@ -88,15 +87,35 @@ struct F32 {
     s = fmaf(__uint_as_float(v.w), __uint_as_float(v.w), s);
     return s;
   }
-  static __device__ __forceinline__ void store_act(elem* rec, int kk, float v) { rec[kk] = v; }
+  static __device__ __forceinline__ void split(float v, elem* hi, elem*) { *hi = v; }
 };
 
-// Activation buffers are K-block-major: the record of (K-block kb, row b)
-// holds P::parts runs of kblk elements (64 bytes each) and sits at element
-// offset (kb * Rp + b) * parts * kblk.
+// Activation buffers (the MFMA B operand of the next projection) are
+// K-block-major: K-block kb of part q (hi / lo) of row b is a 64-byte run at
+// element offset ((kb * parts + q) * Rp + b) * kblk, Rp = padded rows.  The
+// 16 rows of one part of one K-block are therefore 1 KiB of consecutive
+// bytes, which is exactly what one 16-byte-per-lane load of a wave reads.
 template <class P>
-__device__ __forceinline__ typename P::elem* act_record(typename P::elem* act, int Rp, int b, int k) {
-  return act + (static_cast<size_t>(k / P::kblk) * Rp + b) * (P::parts * P::kblk);
+__device__ __forceinline__ size_t act_offset(int Rp, int b, int k, int part) {
+  return (static_cast<size_t>(k / P::kblk * P::parts + part) * Rp + b) * P::kblk + k % P::kblk;
+}
+
+// A K tile of the KV cache (16 positions x head_dim) is stored in MFMA
+// fragment order, as the A operand of scores = K . q^T: fragment c covers
+// dims [c * kblk, (c + 1) * kblk), lane t + 16 g holds position t and dims
+// c * kblk + g * per16 + j, j < per16.  One fragment is 1 KiB of consecutive
+// bytes, so each wave load of a K tile is fully coalesced.
+template <class P>
+__device__ __forceinline__ int ktile_offset(int t, int dd) {
+  return ((dd / P::kblk) * 64 + ((dd % P::kblk) / P::per16) * 16 + t) * P::per16 + dd % P::per16;
+}
+
+template <class P>
+__device__ __forceinline__ void act_store(typename P::elem* act, int Rp, int b, int k, float v) {
+  typename P::elem hi, lo;
+  P::split(v, &hi, &lo);
+  act[act_offset<P>(Rp, b, k, 0)] = hi;
+  if constexpr (P::parts == 2) act[act_offset<P>(Rp, b, k, 1)] = lo;
 }
 
 // ---------------------------------------------------------------------------

@@ -6,19 +6,22 @@
 // below the MFMA ridge).  MFMA is used as the dot-product engine because the
 // tiles come straight from HBM in the operand layout, not because the
 // kernel needs its throughput:
-//   * one workgroup per 16-row output tile; its waves split the K-blocks, each
-//     streaming contiguous 1 KiB weight fragments with 16-byte loads;
-//   * the activations (rows x K, K-block-major records of 64-byte runs, see
-//     act_record) are the MFMA B operand: a lane reads 16 contiguous bytes of
-//     one row, and rows past the batch are not read at all, so a batch of one
-//     reads one row;
+//   * one work-group per RT 16-row output tiles; its waves split the K-blocks,
+//     each streaming contiguous 1 KiB weight fragments with 16-byte loads;
+//   * the activations (rows x K, K-block-major, see act_offset) are the MFMA
+//     B operand: one wave load reads 1 KiB of consecutive bytes (16 rows x 64
+//     bytes of one part), and lanes of rows past the batch re-read row 0, so
+//     a batch of one moves one row's bytes;
+//   * a work-group may own RT row tiles, so each activation fragment feeds RT
+//     weight fragments (fewer activation bytes per weight byte);
 //   * bf16 activations come as hi + lo parts (two MFMAs per fragment), which
 //     keeps the activation side of every product near fp32 precision;
 //   * per-wave accumulators are summed through LDS in a fixed order, so the
 //     result is bitwise reproducible.
 // RMSNorm (unit gains) of the input is fused: the sum of squares of each row
-// is accumulated from the activation fragments already in registers, and
-// 1/sqrt(mean + eps) scales the accumulator in the epilogue.
+// is accumulated from the activation fragments already in registers (on
+// MFMA, see k_stream_gemm), and 1/sqrt(mean + eps) scales the accumulator in
+// the epilogue.
 #pragma once
 
 #include "device_common.h"
@@ -33,72 +36,162 @@ struct RowSlotPos {
   int pos[kRows];
 };
 
-template <class P, int JT, int WAVES, class Epi>
+// Fragments each wave loads per pipeline stage, by MFMA work per K-block
+// (row tiles x activation tiles x parts): more in flight when registers allow.
+template <int XW>
+struct StreamDepth {
+  static constexpr int value = XW <= 2 ? 8 : XW <= 4 ? 4 : 2;
+};
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Weight fragment load; streaming (nontemporal) loads keep the once-read
+// weights from displacing activations in the caches.
+template <bool kStream>
+__device__ __forceinline__ uint4 load_weight(const uint4* p) {
+  if constexpr (kStream) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  } else {
+    return *p;
+  }
+}
+
+// One work-group computes RT consecutive 16-row output tiles for all rows;
+// its WAVES waves split the K-blocks, and each activation fragment a wave
+// loads feeds RT weight fragments.
+template <class P, int JT, int RT, int UH>
+struct StreamStage {
+  uint4 a[UH][RT];                 // weight fragments
+  uint4 x[UH][JT][P::parts];       // activation fragments
+};
+
+// Diagonal of the Gram accumulator g = X^T X of one 16-row activation tile,
+// i.e. the row's sum of squares, for the row of this lane's column.  The
+// diagonal entry of column c sits in lane c + 16 * (c / 4), register c % 4.
+__device__ __forceinline__ float gram_diagonal(const f32x4_t& gm, int lane) {
+  const int c = lane & 15;
+  const float cand = (c & 3) == 0 ? gm[0] : (c & 3) == 1 ? gm[1] : (c & 3) == 2 ? gm[2] : gm[3];
+  return __shfl(cand, c + 16 * (c >> 2));
+}
+
+// One work-group computes RT consecutive 16-row output tiles for all rows;
+// its WAVES waves split the K-blocks, and each activation fragment a wave
+// loads feeds RT weight fragments.  Loads are software-pipelined: a wave
+// issues the next stage of UH K-blocks before computing the current one, so
+// its requests stay in flight while it computes.  For epilogues that apply
+// RMSNorm, the rows' sums of squares come from MFMA too: the Gram product
+// X^T X of each activation fragment with itself (hi.hi + hi.lo + lo.hi)
+// has them on its diagonal.
+template <class P, int JT, int WAVES, class Epi, int RT = 1, int U = StreamDepth<RT * JT * P::parts>::value,
+          bool kStream = false>
 __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X,
                                                             int KB, int Rp, int n_rows, Epi epi) {
-  const int nt = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int PARTS = P::parts;
+  constexpr int UH = U / 2 > 0 ? U / 2 : 1;
+  using Stage = StreamStage<P, JT, RT, UH>;
+  const int nt0 = blockIdx.x * RT;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int kb0 = (KB * wave) / WAVES, kb1 = (KB * (wave + 1)) / WAVES;
-  f32x4_t acc[JT];
-  float ssq[JT];
+  f32x4_t acc[RT][JT], gram[JT];
 #pragma unroll
   for (int j = 0; j < JT; ++j) {
-    acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    ssq[j] = 0.f;
+#pragma unroll
+    for (int t = 0; t < RT; ++t) acc[t][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    gram[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-  const uint4* wp = W + static_cast<size_t>(nt) * KB * 64 + lane;
-  // Activation record (kb, row) = PARTS runs of 64 bytes; lane reads 16 bytes of each.
-  constexpr int PARTS = P::parts;
-  constexpr int REC = 4 * PARTS;  // uint4 per record
-  const uint4* xp = X + (lane & 15) * REC + (lane >> 4);
-  bool rv[JT];  // rows past n_rows are never read: their lanes feed zeros
+  const uint4* wp = W + static_cast<size_t>(nt0) * KB * 64 + lane;
+  const size_t wtile = static_cast<size_t>(KB) * 64;  // uint4 per row tile
+  // Lanes of rows past n_rows read row 0 instead (the same cache lines as a
+  // valid lane, so no extra traffic); their accumulator columns are never
+  // stored, and MFMA columns do not mix, so the values they read do not matter.
+  int xoff[JT];
 #pragma unroll
-  for (int j = 0; j < JT; ++j) rv[j] = 16 * j + (lane & 15) < n_rows;
-  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-  constexpr int XW = JT * PARTS;
-  constexpr int U = XW <= 2 ? 8 : XW <= 4 ? 4 : 2;
-  int kb = kb0;
-  for (; kb + U <= kb1; kb += U) {
-    uint4 a[U], x[U][JT][PARTS];
+  for (int j = 0; j < JT; ++j) {
+    const int b = 16 * j + (lane & 15);
+    xoff[j] = (b < n_rows ? b : 0) * 4 + (lane >> 4);
+  }
+  const size_t xpart = static_cast<size_t>(Rp) * 4;  // uint4 per (K-block, part)
+
+  auto load = [&](Stage& st, int kb) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      a[u] = wp[static_cast<size_t>(kb + u) * 64];
+    for (int u = 0; u < UH; ++u) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t) st.a[u][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb + u) * 64);
 #pragma unroll
       for (int j = 0; j < JT; ++j)
 #pragma unroll
-        for (int q = 0; q < PARTS; ++q)
-          x[u][j][q] = rv[j] ? xp[(static_cast<size_t>(kb + u) * Rp + 16 * j) * REC + 4 * q] : zero;
+        for (int q = 0; q < PARTS; ++q) st.x[u][j][q] = X[(static_cast<size_t>(kb + u) * PARTS + q) * xpart + xoff[j]];
     }
+  };
+  auto compute = [&](const Stage& st) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < UH; ++u) {
 #pragma unroll
       for (int j = 0; j < JT; ++j) {
 #pragma unroll
-        for (int q = 0; q < PARTS; ++q) acc[j] = P::mma(acc[j], a[u], x[u][j][q]);
-        if constexpr (Epi::kNorm) ssq[j] += P::sumsq(x[u][j][0], x[u][j][PARTS - 1]);
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+          for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[u][t], st.x[u][j][q]);
+        if constexpr (Epi::kNorm) {
+          gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
+          if constexpr (PARTS == 2) {
+            gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][1]);
+            gram[j] = P::mma(gram[j], st.x[u][j][1], st.x[u][j][0]);
+          }
+        }
+      }
+    }
+  };
+
+  const int nstage = (kb1 - kb0) / UH;
+  Stage s0, s1;
+  if (nstage > 0) load(s0, kb0);
+  for (int c = 0; c < nstage; c += 2) {
+    if (c + 1 < nstage) load(s1, kb0 + (c + 1) * UH);
+    compute(s0);
+    if (c + 1 < nstage) {
+      if (c + 2 < nstage) load(s0, kb0 + (c + 2) * UH);
+      compute(s1);
+    }
+  }
+  for (int kb = kb0 + nstage * UH; kb < kb1; ++kb) {
+    Stage& st = s0;
+#pragma unroll
+    for (int t = 0; t < RT; ++t) st.a[0][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb) * 64);
+#pragma unroll
+    for (int j = 0; j < JT; ++j)
+#pragma unroll
+      for (int q = 0; q < PARTS; ++q) st.x[0][j][q] = X[(static_cast<size_t>(kb) * PARTS + q) * xpart + xoff[j]];
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[0][t], st.x[0][j][q]);
+      if constexpr (Epi::kNorm) {
+        gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
+        if constexpr (PARTS == 2) {
+          gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][1]);
+          gram[j] = P::mma(gram[j], st.x[0][j][1], st.x[0][j][0]);
+        }
       }
     }
   }
-  for (; kb < kb1; ++kb) {
-    const uint4 a = wp[static_cast<size_t>(kb) * 64];
+  float ssq[JT];
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
-      uint4 x[PARTS];
-#pragma unroll
-      for (int q = 0; q < PARTS; ++q) x[q] = rv[j] ? xp[(static_cast<size_t>(kb) * Rp + 16 * j) * REC + 4 * q] : zero;
-#pragma unroll
-      for (int q = 0; q < PARTS; ++q) acc[j] = P::mma(acc[j], a, x[q]);
-      if constexpr (Epi::kNorm) ssq[j] += P::sumsq(x[0], x[PARTS - 1]);
-    }
-  }
+  for (int j = 0; j < JT; ++j) ssq[j] = Epi::kNorm ? gram_diagonal(gram[j], lane) : 0.f;
   if constexpr (WAVES > 1) {
-    __shared__ float red[WAVES - 1][JT][5][64];
+    __shared__ float red[WAVES - 1][JT][4 * RT + 1][64];
     if (wave > 0) {
 #pragma unroll
       for (int j = 0; j < JT; ++j) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) red[wave - 1][j][c][lane] = acc[j][c];
-        red[wave - 1][j][4][lane] = ssq[j];
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) red[wave - 1][j][4 * t + c][lane] = acc[t][j][c];
+        red[wave - 1][j][4 * RT][lane] = ssq[j];
       }
     }
     __syncthreads();
@@ -107,38 +200,32 @@ __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restr
 #pragma unroll
       for (int j = 0; j < JT; ++j) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[j][c] += red[w][j][c][lane];
-        ssq[j] += red[w][j][4][lane];
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[t][j][c] += red[w][j][4 * t + c][lane];
+        ssq[j] += red[w][j][4 * RT][lane];
       }
     }
   }
-  if constexpr (Epi::kNorm) {
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
-      ssq[j] += __shfl_xor(ssq[j], 16);
-      ssq[j] += __shfl_xor(ssq[j], 32);
-    }
-  }
-  epi.template apply<JT>(nt, acc, ssq, lane);
+  for (int t = 0; t < RT; ++t) epi.template apply<JT>(nt0 + t, acc[t], ssq, lane);
 }
 
-// Stores four consecutive features n0..n0+3 of row b into a K-block-major activation buffer.
+// Stores four consecutive features n0..n0+3 of row b into an activation buffer.
 template <class P>
 __device__ __forceinline__ void store_act4(typename P::elem* act, int Rp, int b, int n0, float v0, float v1, float v2,
                                            float v3) {
-  typename P::elem* rec = act_record<P>(act, Rp, b, n0);
-  const int kk = n0 % P::kblk;
-  P::store_act(rec, kk, v0);
-  P::store_act(rec, kk + 1, v1);
-  P::store_act(rec, kk + 2, v2);
-  P::store_act(rec, kk + 3, v3);
+  act_store<P>(act, Rp, b, n0, v0);
+  act_store<P>(act, Rp, b, n0 + 1, v1);
+  act_store<P>(act, Rp, b, n0 + 2, v2);
+  act_store<P>(act, Rp, b, n0 + 3, v3);
 }
 
 // QKV projection -> RMSNorm scale -> RoPE on q and k -> q to the attention
 // input, k and v appended to the paged KV cache at the row's position.
-// K block layout [block][kv_head][16 positions][head_dim]; V is stored
-// transposed per block, [block][kv_head][head_dim][16 positions], so the
-// attention kernel reads 4 consecutive positions of one dimension as one
+// Per (block, KV head) the K tile is 16 positions x head_dim in MFMA fragment
+// order (ktile_offset); V is stored transposed, [head_dim][16 positions], so
+// the attention kernel reads 4 consecutive positions of one dimension as one
 // MFMA operand.
 template <class P>
 struct EpiQKV {
@@ -182,7 +269,7 @@ struct EpiQKV {
       const int off = p & 15;
       if (n0 < qr + kr) {
         const int m = n0 - qr, kvh = m / hd, dd = m % hd;
-        typename P::elem* dst = kc + ((static_cast<size_t>(blk) * Hkv + kvh) * 16 + off) * hd + dd;
+        typename P::elem* dst = kc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd + ktile_offset<P>(off, dd);
         dst[0] = P::from_f32(v0);
         dst[1] = P::from_f32(v1);
         dst[2] = P::from_f32(v2);
@@ -247,9 +334,8 @@ struct EpiSwiGLU {
       const float g0 = acc[j][0] * s, g1 = acc[j][1] * s, u0 = acc[j][2] * s, u1 = acc[j][3] * s;
       const float h0 = g0 / (1.f + __expf(-g0)) * u0;
       const float h1 = g1 / (1.f + __expf(-g1)) * u1;
-      typename P::elem* rec = act_record<P>(act, Rp, b, j0);
-      P::store_act(rec, j0 % P::kblk, h0);
-      P::store_act(rec, j0 % P::kblk + 1, h1);
+      act_store<P>(act, Rp, b, j0, h0);
+      act_store<P>(act, Rp, b, j0 + 1, h1);
     }
   }
 };

@@ -162,18 +162,35 @@ struct RowSet {
   int tok[kRows];
 };
 
+// Launch shape of a projection (measured on MI355X): projections with many
+// 16-row tiles use 4-wave work-groups, two tiles per work-group once more
+// than 8 rows share each activation fragment; narrow projections (fewer than
+// 512 tiles, e.g. the O and down projections) use one tile per work-group
+// and more waves, so every CU streams its tile with enough loads in flight.
+// Waves per work-group of a narrow projection; wider row sets need the
+// registers of fewer waves.
+template <int JT>
+constexpr int kNarrowWaves = JT == 1 ? 16 : JT <= 4 ? 8 : 4;
+
 template <class P, class Epi>
 spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int KB, int JT, const Epi& epi) {
   const uint4* w = reinterpret_cast<const uint4*>(W);
   const uint4* x = reinterpret_cast<const uint4*>(X);
   const int Rp = 16 * JT;
-  const bool wide = NT >= 512 || JT >= 8;  // 8-wave variants of JT = 8 would spill
-#define SPR_GEMM_CASE(JTV)                                                                         \
-  case JTV:                                                                                        \
-    if (wide)                                                                                      \
-      k_stream_gemm<P, JTV, 4, Epi><<<NT, 256, 0, m->st>>>(w, x, KB, Rp, epi.n_rows, epi);          \
-    else                                                                                           \
-      k_stream_gemm<P, JTV, 8, Epi><<<NT, 512, 0, m->st>>>(w, x, KB, Rp, epi.n_rows, epi);          \
+  const int n = epi.n_rows;
+  const bool narrow = NT < 512;
+  const bool pair = !narrow && (n > 8 || JT >= 2) && NT % 2 == 0 && JT <= 4;
+#define SPR_GEMM_CASE(JTV)                                                                               \
+  case JTV:                                                                                              \
+    if (narrow)                                                                                          \
+      k_stream_gemm<P, JTV, kNarrowWaves<JTV>, Epi, 1, StreamDepth<JTV * P::parts>::value, true>        \
+          <<<NT, kNarrowWaves<JTV> * 64, 0, m->st>>>(w, x, KB, Rp, n, epi);                              \
+    else if (pair)                                                                                       \
+      k_stream_gemm<P, JTV, 4, Epi, 2, StreamDepth<2 * JTV * P::parts>::value, true>                    \
+          <<<NT / 2, 256, 0, m->st>>>(w, x, KB, Rp, n, epi);                                             \
+    else                                                                                                 \
+      k_stream_gemm<P, JTV, 4, Epi, 1, StreamDepth<JTV * P::parts>::value, true>                        \
+          <<<NT, 256, 0, m->st>>>(w, x, KB, Rp, n, epi);                                                 \
     break;
   switch (JT) {
     SPR_GEMM_CASE(1)
@@ -232,16 +249,20 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     SPR_LAUNCHED(m, "k_embed");
   }
 
-  // KV splits: enough (row, head, split) work-groups to cover the chip.
+  // KV splits: a work-group covers bps blocks of one (row, KV head), 4 waves
+  // of bps / 4 blocks each.  Waves get 1..4 blocks so that there are about
+  // 4096 of them (16 per CU) whenever the context allows, and at most
+  // kSplitsMax splits per (row, head).
   int total_blk = 0, max_blk = 0;
   for (int r = 0; r < n; ++r) {
     const int nb = (rs.pos[r] + 1 + 15) / 16;
     total_blk += nb;
     if (nb > max_blk) max_blk = nb;
   }
-  int bps = ceil_div(total_blk * d.Hkv, 1024);
-  if (bps < 4) bps = 4;
-  if (ceil_div(max_blk, bps) > kSplitsMax) bps = ceil_div(max_blk, kSplitsMax);
+  int bpw = ceil_div(total_blk * d.Hkv, 4096);
+  bpw = bpw < 1 ? 1 : bpw > 4 ? 4 : bpw;
+  if (ceil_div(max_blk, 4 * bpw) > kSplitsMax) bpw = ceil_div(ceil_div(max_blk, kSplitsMax), 4);
+  const int bps = 4 * bpw;
   const int max_splits = ceil_div(max_blk, bps);
 
   spr_status st;
@@ -319,6 +340,41 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     SPR_LAUNCHED(m, "k_argmax_final");
   }
   return SPR_OK;
+}
+
+// Launches one projection of `layer` over n rows (see spr_time_projection).
+template <class P>
+spr_status launch_projection(spr_model* m, int projection, int layer, int n) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  const int JT = n <= 16 ? 1 : n <= 32 ? 2 : n <= 64 ? 4 : 8;
+  const int Rp = 16 * JT;
+  using E = typename P::elem;
+  switch (projection) {
+    case 1: {
+      EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      return launch_gemm<P>(m, d.nt_o, p.wo(layer), p.act(1), d.kb_o, JT, e);
+    }
+    case 2: {
+      EpiSwiGLU<P> e{n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(1))};
+      return launch_gemm<P>(m, d.nt_13, p.w13(layer), p.act(0), d.kb_d, JT, e);
+    }
+    case 3: {
+      EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      return launch_gemm<P>(m, d.nt_2, p.w2(layer), p.act(1), d.kb_f, JT, e);
+    }
+    default: {
+      EpiLogits<P> e{};
+      e.n_rows = n;
+      e.V = d.V;
+      e.dnorm = d.d;
+      e.eps = d.eps;
+      e.logits = nullptr;
+      e.part = p.amax();
+      for (int r = 0; r < kRows; ++r) e.out_row[r] = -1;
+      return launch_gemm<P>(m, d.nt_lm, p.wlm(), p.act(0), d.kb_d, JT, e);
+    }
+  }
 }
 
 spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
@@ -556,6 +612,41 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
                                                            which_of[tensor], row0, nrows, out);
   }
   SPR_LAUNCHED(m, "export");
+  return SPR_OK;
+}
+
+spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (avg_us == nullptr) return fail(SPR_ERR_INVALID_ARG, "time_projection: avg_us must not be null");
+  if (projection < 1 || projection > 4)
+    return fail(SPR_ERR_INVALID_ARG, "time_projection: projection must be 1 (O), 2 (gate/up), 3 (down) or 4 (LM head)");
+  if (n_rows < 1 || n_rows > kRows || reps < 1 || reps > 100000)
+    return fail(SPR_ERR_INVALID_ARG, "time_projection: n_rows in [1, 128] and reps in [1, 100000]");
+  hipEvent_t e0, e1;
+  SPR_HIP(m, hipEventCreate(&e0));
+  hipError_t e = hipEventCreate(&e1);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return hip_fail(m, "hipEventCreate", e);
+  }
+  e = hipEventRecord(e0, m->st);
+  // Launch r uses layer r mod n_layers, so the weights streamed are the whole
+  // model's share of this projection, as in a decode step, and a matrix that
+  // would fit in the last-level cache is not re-read from it.
+  for (int r = 0; r < reps && e == hipSuccess && st == SPR_OK; ++r)
+    st = m->d.dtype == SPR_BF16 ? launch_projection<BF16>(m, projection, r % m->d.L, n_rows)
+                                : launch_projection<F32>(m, projection, r % m->d.L, n_rows);
+  if (e == hipSuccess && st == SPR_OK) e = hipEventRecord(e1, m->st);
+  if (e == hipSuccess && st == SPR_OK) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess && st == SPR_OK) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (st != SPR_OK) return st;
+  if (e != hipSuccess) return hip_fail(m, "time_projection", e);
+  *avg_us = 1000.f * ms / static_cast<float>(reps);
   return SPR_OK;
 }
 
