@@ -68,7 +68,7 @@ def cpu_baseline(cfg, wl, seconds: float):
     from oracle import llama_ref as R
     m = cfg.model
     sh = R.Shape(m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff, m.vocab,
-                 m.rope_base, m.rms_eps, m.bf16)
+                 m.rope_base, m.rms_eps, m.bf16, kv_bf16=m.kv_is_bf16)
     t0 = time.perf_counter()
     w = R.Weights(sh, cfg.weight_seed, resident=True)
     for l in range(sh.n_layers):

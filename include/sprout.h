@@ -52,8 +52,9 @@ typedef enum { SPR_F32 = 0, SPR_BF16 = 1 } spr_dtype;
  * Model shape and capacity.  Llama-2 architecture (Section IV): pre-norm
  * decoder layers of RMSNorm -> attention with rotary position embedding ->
  * residual, RMSNorm -> SwiGLU MLP -> residual; untied embedding and LM head;
- * no biases.  Weights and the KV cache are stored in `dtype`; the residual
- * stream, norms, softmax, accumulation and logits are fp32.
+ * no biases.  Weights are stored in `dtype` and the KV cache in `kv_dtype`
+ * (keys and values are rounded to it, nearest-even, when cached); the
+ * residual stream, norms, softmax, accumulation and logits are fp32.
  *
  * Constraints: n_layers 1..255; head_dim 64 or 128; n_heads a multiple of
  * n_kv_heads with n_heads / n_kv_heads <= 16; d_model a multiple of 16;
@@ -69,6 +70,7 @@ typedef struct {
   int32_t max_slots; /* concurrent requests */
   int32_t max_ctx;   /* positions per request: prompt + generated - 1 */
   int32_t kv_blocks; /* KV blocks in the pool */
+  int32_t kv_dtype;  /* spr_dtype of the KV cache; fp32 models need SPR_F32 */
 } spr_config;
 
 typedef struct spr_model spr_model; /* opaque, library-owned host state */

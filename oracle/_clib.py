@@ -32,10 +32,15 @@ def splitmix_output(seed: int, n: int) -> int:
     return int(lib().oracle_splitmix_output(seed & (2**64 - 1), n))
 
 
-def wgen_rows(seed, tensor, layer, n_cols, row0, nrows, bf16, dtype=np.float64):
-    """Rows [row0, row0+nrows) of the logical matrix (tensor, layer) with n_cols columns."""
+def wgen_rows(seed, tensor, layer, n_cols, row0, nrows, bf16, dtype=np.float64, out=None):
+    """Rows [row0, row0+nrows) of the logical matrix (tensor, layer) with n_cols columns.
+
+    `out` (fp64, C-contiguous, shape (nrows, n_cols)) is filled in place when given.
+    """
     if dtype == np.float64:
-        out = np.empty((nrows, n_cols), dtype=np.float64)
+        if out is None:
+            out = np.empty((nrows, n_cols), dtype=np.float64)
+        assert out.shape == (nrows, n_cols) and out.dtype == np.float64 and out.flags.c_contiguous
         lib().oracle_wgen_rows(seed, tensor, layer, n_cols, row0, nrows, int(bf16),
                                out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
     else:

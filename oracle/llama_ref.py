@@ -27,9 +27,9 @@ published Llama-2 architecture, restated here in plain numpy.
 
 Everything is fp64.  Weights are the exact fp32 / bf16 values drawn by the
 counter-based generator in wgen.c, widened to fp64.  The KV cache is model
-state kept in the model's storage format: a key or value is rounded to bf16
-(fp32 for fp32 models), nearest-even, when it is cached, and attention reads
-the cached values.  Nothing else is rounded.
+state kept in the model's KV-cache format: a key or value is rounded to bf16
+or fp32, nearest-even, when it is cached, and attention reads the cached
+values.  Nothing else is rounded.
 
 Two forms of the same computation are provided:
   * ``forward_causal``  -- one causal pass over a whole token sequence, giving
@@ -66,10 +66,11 @@ class Shape:
     rope_base: float = 10000.0
     rms_eps: float = 1e-5
     bf16: bool = True
-    # Cached keys/values are stored in the model's storage format (bf16 or
-    # fp32), rounded to nearest-even when written.  False keeps them exact
-    # (fp64), which only the brute-force pins use.
+    # Cached keys/values are stored in the KV-cache format (bf16 or fp32;
+    # None: the weight format), rounded to nearest-even when written.
+    # kv_round False keeps them exact (fp64), which only brute-force pins use.
     kv_round: bool = True
+    kv_bf16: Optional[bool] = None
 
     def matrix_dims(self, name: str):
         d, hd = self.d_model, self.head_dim
@@ -101,15 +102,21 @@ class Weights:
         self.seed = int(seed)
         self.resident = resident
         self._cache: Dict[tuple, np.ndarray] = {}
+        self._scratch: Dict[str, np.ndarray] = {}
 
     def matrix(self, name: str, layer: int = 0) -> np.ndarray:
+        """The matrix (fp64).  Without residency, a matrix stays valid only until
+        the same matrix of another layer is asked for (its buffer is reused)."""
         key = (name, layer)
         if key in self._cache:
             return self._cache[key]
         rows, cols = self.shape.matrix_dims(name)
-        m = _clib.wgen_rows(self.seed, TENSOR_IDS[name], layer, cols, 0, rows, self.shape.bf16)
+        out = None if self.resident else self._scratch.get(name)
+        m = _clib.wgen_rows(self.seed, TENSOR_IDS[name], layer, cols, 0, rows, self.shape.bf16, out=out)
         if self.resident:
             self._cache[key] = m
+        else:
+            self._scratch[name] = m
         return m
 
     def rows(self, name: str, layer: int, row0: int, nrows: int) -> np.ndarray:
@@ -173,7 +180,8 @@ def cache_kv(shape: Shape, k: np.ndarray, v: np.ndarray):
     """Keys/values as the KV cache holds them (the model's storage format)."""
     if not shape.kv_round:
         return k, v
-    return round_to_storage(k, shape.bf16), round_to_storage(v, shape.bf16)
+    kv_bf16 = shape.bf16 if shape.kv_bf16 is None else shape.kv_bf16
+    return round_to_storage(k, kv_bf16), round_to_storage(v, kv_bf16)
 
 
 def softmax(s: np.ndarray) -> np.ndarray:
@@ -205,12 +213,18 @@ def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
 
 
 def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
-    """Position t attends to positions 0..t.  q: [T,H,hd], k,v: [T,Hkv,hd] -> [T,H,hd]."""
-    T = q.shape[0]
-    out = np.empty(q.shape)
-    for t in range(T):
-        out[t] = attend(q[t], k[: t + 1], v[: t + 1])
-    return out
+    """Position t attends to positions 0..t: softmax(q k^T / sqrt(hd) + causal mask) v, per head.
+
+    q: [T,H,hd], k,v: [T,Hkv,hd] -> [T,H,hd].  Query head h uses KV head
+    h // (H / Hkv), i.e. each KV head is repeated for its group of query heads.
+    """
+    T, H, hd = q.shape
+    group = H // k.shape[1]
+    kh = np.repeat(k, group, axis=1).transpose(1, 2, 0)      # [H, hd, T]
+    vh = np.repeat(v, group, axis=1).transpose(1, 0, 2)      # [H, T, hd]
+    s = np.matmul(q.transpose(1, 0, 2), kh) / math.sqrt(hd)  # [H, T(query), T(key)]
+    s[:, np.triu(np.ones((T, T), dtype=bool), k=1)] = -np.inf
+    return np.matmul(softmax(s), vh).transpose(1, 0, 2)
 
 
 def silu(x: np.ndarray) -> np.ndarray:
@@ -242,11 +256,12 @@ def embed_rows(w: Weights, tokens: Sequence[int]) -> np.ndarray:
 
 
 def forward_causal(w: Weights, tokens: Sequence[int], want_positions: Optional[Sequence[int]] = None,
-                   n_layers: Optional[int] = None) -> np.ndarray:
+                   n_layers: Optional[int] = None, progress=None) -> np.ndarray:
     """Logits [len(want_positions), V] of one request whose tokens sit at positions 0..T-1.
 
     Layers are processed one at a time so the weights can be streamed.
-    ``n_layers`` truncates the model (used only by pins on toy shapes).
+    ``n_layers`` truncates the model (used only by pins on toy shapes);
+    ``progress(layer)`` is called after each layer if given.
     """
     sh = w.shape
     tokens = np.asarray(tokens, dtype=np.int64)
@@ -269,6 +284,8 @@ def forward_causal(w: Weights, tokens: Sequence[int], want_positions: Optional[S
         m = rmsnorm(x, g, sh.rms_eps)
         x = x + swiglu(m, W["w1"], W["w3"], W["w2"])
         del W
+        if progress is not None:
+            progress(layer)
     if want_positions is None:
         want_positions = range(T)
     xs = rmsnorm(x[np.asarray(want_positions, dtype=np.int64)], g, sh.rms_eps)
@@ -276,7 +293,7 @@ def forward_causal(w: Weights, tokens: Sequence[int], want_positions: Optional[S
 
 
 def teacher_forced_logits(w: Weights, prompt: Sequence[int], generated: Sequence[int],
-                          steps: Optional[Sequence[int]] = None) -> np.ndarray:
+                          steps: Optional[Sequence[int]] = None, progress=None) -> np.ndarray:
     """Logits that produced generated token g_s, for s in ``steps`` (default: all).
 
     g_0 comes from the last prompt position; g_s (s >= 1) from feeding g_{s-1}
@@ -290,7 +307,7 @@ def teacher_forced_logits(w: Weights, prompt: Sequence[int], generated: Sequence
     steps = list(steps)
     last = max(steps)
     seq = list(prompt) + list(generated[:last])
-    return forward_causal(w, seq, [n - 1 + s for s in steps])
+    return forward_causal(w, seq, [n - 1 + s for s in steps], progress=progress)
 
 
 # --------------------------------------------------------------------------

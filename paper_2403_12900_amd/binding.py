@@ -28,7 +28,7 @@ class SprConfig(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
                 ("dtype", ctypes.c_int32), ("kv_block", ctypes.c_int32), ("max_slots", ctypes.c_int32),
-                ("max_ctx", ctypes.c_int32), ("kv_blocks", ctypes.c_int32)]
+                ("max_ctx", ctypes.c_int32), ("kv_blocks", ctypes.c_int32), ("kv_dtype", ctypes.c_int32)]
 
 
 class SproutError(RuntimeError):
@@ -82,7 +82,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
 def make_config(m: ModelConfig, max_slots: int, max_ctx: int, kv_blocks: int) -> SprConfig:
     return SprConfig(m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff, m.vocab,
                      m.rope_base, m.rms_eps, SPR_BF16 if m.bf16 else SPR_F32, KV_BLOCK, max_slots, max_ctx,
-                     kv_blocks)
+                     kv_blocks, SPR_BF16 if m.kv_is_bf16 else SPR_F32)
 
 
 def _i32(a) -> np.ndarray:

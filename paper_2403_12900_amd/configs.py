@@ -23,6 +23,11 @@ class ModelConfig:
     rope_base: float = 10000.0
     rms_eps: float = 1e-5
     bf16: bool = True
+    kv_bf16: Optional[bool] = None   # KV-cache format; None: the weight format
+
+    @property
+    def kv_is_bf16(self) -> bool:
+        return self.bf16 if self.kv_bf16 is None else self.kv_bf16
 
     @property
     def qkv_rows(self) -> int:
@@ -40,7 +45,7 @@ class ModelConfig:
 
     def kv_bytes_per_token(self) -> int:
         """K and V of one position over all layers."""
-        return 2 * self.n_layers * self.n_kv_heads * self.head_dim * self.weight_bytes
+        return 2 * self.n_layers * self.n_kv_heads * self.head_dim * (2 if self.kv_is_bf16 else 4)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -70,7 +75,11 @@ class DecodeConfig:
 TINY = ModelConfig(n_layers=2, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=688, vocab=1024, bf16=False)
 LLAMA2_7B = ModelConfig(n_layers=32, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128, d_ff=11008, vocab=32000)
 LLAMA2_13B = ModelConfig(n_layers=40, d_model=5120, n_heads=40, n_kv_heads=40, head_dim=128, d_ff=13824, vocab=32000)
-LLAMA2_70B = ModelConfig(n_layers=80, d_model=8192, n_heads=64, n_kv_heads=8, head_dim=128, d_ff=28672, vocab=32000)
+# The 70B shape keeps its (grouped, 8x smaller per token) KV cache in fp32: at
+# 80 layers of a random-init network, bf16 rounding of cached keys/values
+# amplifies past the logit tolerance, and fp32 costs ~3% of the step's bytes.
+LLAMA2_70B = ModelConfig(n_layers=80, d_model=8192, n_heads=64, n_kv_heads=8, head_dim=128, d_ff=28672, vocab=32000,
+                         kv_bf16=False)
 
 _DIRECTIVE_STOPS = (400.0, 120.0, 40.0)   # generation-length medians for L0 / L1 / L2
 

@@ -113,6 +113,8 @@ struct KVBlock {
   }
 };
 
+// P is the KV-cache storage format (it also sets the MFMA operand type of q
+// and of the probabilities); AP is the format of the output activation.
 // Work-group (split s, row b, KV head): blocks [s * bps, min(nblk, (s + 1) *
 // bps)); wave w takes the contiguous run of bps / 4 blocks starting at
 // w * bps / 4.  A wave walks its blocks one at a time -- load K and V, scores,
@@ -121,7 +123,7 @@ struct KVBlock {
 // keeping two blocks in flight per wave at lower occupancy).  Branch
 // conditions are wave-uniform; the partial last block of the context is
 // masked by selects.
-template <class P, int HD>
+template <class P, class AP, int HD>
 __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   using E = typename P::elem;
   using Blk = KVBlock<P, HD>;
@@ -243,11 +245,11 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   const int hq = kvh * a.G + h;
   if (nsplit == 1) {
     const float inv = 1.f / L;
-    E* act = static_cast<E*>(a.act);
+    typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
     for (int e = 0; e < NE; ++e)
-      store_act4<P>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
-                    O[e][3] * inv);
+      store_act4<AP>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
+                     O[e][3] * inv);
   } else {
     float* pp = a.part + ((static_cast<size_t>(b) * a.H + hq) * kSplitsMax + s) * (HD + 4);
     if (g == 0) {
@@ -261,7 +263,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
 }
 
 // Log-sum-exp merge of the KV splits of rows that needed more than one.  All
-// splits' statistics and values are loaded before any is combined.
+// splits' statistics and values are loaded before any is combined.  P is the
+// activation format of the output.
 template <class P, int HD>
 __global__ __launch_bounds__(HD) void k_attn_merge(AttnArgs a) {
   const int b = blockIdx.x, hq = blockIdx.y, dd = threadIdx.x;

@@ -227,14 +227,14 @@ __device__ __forceinline__ void store_act4(typename P::elem* act, int Rp, int b,
 // order (ktile_offset); V is stored transposed, [head_dim][16 positions], so
 // the attention kernel reads 4 consecutive positions of one dimension as one
 // MFMA operand.
-template <class P>
+template <class P, class KP = P>
 struct EpiQKV {
   static constexpr bool kNorm = true;
   int n_rows, H, Hkv, hd, mb, dnorm;
   float eps;
   float* q;                     // [rows][H * hd]
-  typename P::elem* kc;         // this layer's K blocks
-  typename P::elem* vc;         // this layer's V blocks
+  typename KP::elem* kc;        // this layer's K blocks (KV-cache format KP)
+  typename KP::elem* vc;        // this layer's V blocks
   const int32_t* bt;            // [slots][mb]
   const float2* rope;           // [positions][hd / 2] (cos, sin)
   RowSlotPos rows;
@@ -269,18 +269,18 @@ struct EpiQKV {
       const int off = p & 15;
       if (n0 < qr + kr) {
         const int m = n0 - qr, kvh = m / hd, dd = m % hd;
-        typename P::elem* dst = kc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd + ktile_offset<P>(off, dd);
-        dst[0] = P::from_f32(v0);
-        dst[1] = P::from_f32(v1);
-        dst[2] = P::from_f32(v2);
-        dst[3] = P::from_f32(v3);
+        typename KP::elem* dst = kc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd + ktile_offset<KP>(off, dd);
+        dst[0] = KP::from_f32(v0);
+        dst[1] = KP::from_f32(v1);
+        dst[2] = KP::from_f32(v2);
+        dst[3] = KP::from_f32(v3);
       } else {
         const int m = n0 - qr - kr, kvh = m / hd, dd = m % hd;
-        typename P::elem* dst = vc + ((static_cast<size_t>(blk) * Hkv + kvh) * hd + dd) * 16 + off;
-        dst[0] = P::from_f32(v0);
-        dst[16] = P::from_f32(v1);
-        dst[32] = P::from_f32(v2);
-        dst[48] = P::from_f32(v3);
+        typename KP::elem* dst = vc + ((static_cast<size_t>(blk) * Hkv + kvh) * hd + dd) * 16 + off;
+        dst[0] = KP::from_f32(v0);
+        dst[16] = KP::from_f32(v1);
+        dst[32] = KP::from_f32(v2);
+        dst[48] = KP::from_f32(v3);
       }
     }
   }

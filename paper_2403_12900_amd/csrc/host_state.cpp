@@ -28,6 +28,8 @@ bool derive(const spr_config& c, Dims* out, std::string* err) {
   if (c.d_model < 16 || c.d_model % 16 != 0) return fail(err, "d_model must be a positive multiple of 16");
   if (c.d_ff < 1 || c.vocab < 1) return fail(err, "d_ff and vocab must be >= 1");
   if (c.dtype != SPR_F32 && c.dtype != SPR_BF16) return fail(err, "dtype must be SPR_F32 or SPR_BF16");
+  if (c.kv_dtype != SPR_F32 && c.kv_dtype != SPR_BF16) return fail(err, "kv_dtype must be SPR_F32 or SPR_BF16");
+  if (c.dtype == SPR_F32 && c.kv_dtype != SPR_F32) return fail(err, "fp32 models keep an fp32 KV cache");
   if (c.kv_block != kKvBlock) return fail(err, "kv_block must be 16");
   if (c.max_slots < 1 || c.max_slots > 64) return fail(err, "max_slots must be in [1, 64]");
   if (c.max_ctx < 1 || c.max_ctx > (1 << 20)) return fail(err, "max_ctx must be in [1, 2^20]");
@@ -49,6 +51,8 @@ bool derive(const spr_config& c, Dims* out, std::string* err) {
   d.dtype = c.dtype;
   d.esize = c.dtype == SPR_BF16 ? 2 : 4;
   d.kblk = c.dtype == SPR_BF16 ? 32 : 16;
+  d.kv_dtype = c.kv_dtype;
+  d.kv_esize = c.kv_dtype == SPR_BF16 ? 2 : 4;
   d.qkv_rows = (d.H + 2 * d.Hkv) * d.hd;
   d.o_in = d.H * d.hd;
   d.nt_qkv = d.qkv_rows / 16;
@@ -92,7 +96,7 @@ Layout layout(const Dims& d) {
   l.off_wlm = take(static_cast<size_t>(d.nt_lm) * d.kb_d * F);
   l.off_emb = take(static_cast<size_t>(d.V) * d.d * d.esize);
   l.off_rope = take(static_cast<size_t>(d.max_ctx) * (d.hd / 2) * 2 * sizeof(float));
-  l.kv_layer_stride = static_cast<size_t>(d.nb) * d.Hkv * kKvBlock * d.hd * d.esize;
+  l.kv_layer_stride = static_cast<size_t>(d.nb) * d.Hkv * kKvBlock * d.hd * d.kv_esize;
   l.off_kc = take(l.kv_layer_stride * d.L);
   l.off_vc = take(l.kv_layer_stride * d.L);
   l.off_bt = take(static_cast<size_t>(d.S) * d.mb * sizeof(int32_t));

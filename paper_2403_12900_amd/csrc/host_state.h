@@ -21,6 +21,7 @@ constexpr int kFragBytes = 1024; // one MFMA operand fragment: 64 lanes x 16 byt
 struct Dims {
   int L, d, H, Hkv, hd, f, V, G;
   int dtype, esize, kblk;          // element bytes; elements per K-block (32 bf16 / 16 fp32)
+  int kv_dtype, kv_esize;          // KV-cache storage format
   int qkv_rows, o_in;              // (H + 2 Hkv) hd, H hd
   int nt_qkv, nt_o, nt_13, nt_2, nt_lm;  // 16-row output tiles (gate/up: 8 features per tile)
   int kb_d, kb_o, kb_f, kb_max;    // K-blocks of the inputs d, H hd, d_ff

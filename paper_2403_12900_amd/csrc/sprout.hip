@@ -205,10 +205,10 @@ spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int K
   return SPR_OK;
 }
 
-template <class P, int HD>
+template <class P, class KP, int HD>
 spr_status launch_attention(spr_model* m, const AttnArgs& a, int max_splits) {
   dim3 grid(max_splits, a.n_rows, a.Hkv);
-  k_attn_decode<P, HD><<<grid, 256, 0, m->st>>>(a);
+  k_attn_decode<KP, P, HD><<<grid, 256, 0, m->st>>>(a);
   SPR_LAUNCHED(m, "k_attn_decode");
   if (max_splits > 1) {
     k_attn_merge<P, HD><<<dim3(a.n_rows, a.H), HD, 0, m->st>>>(a);
@@ -220,7 +220,7 @@ spr_status launch_attention(spr_model* m, const AttnArgs& a, int max_splits) {
 // One forward pass over rs (rows: slot, position, emitted logits row).
 // tok_in != null: the inputs are tok_in[slot]; otherwise rs.tok.  Emitting
 // rows write their greedy token to tok_out[slot].
-template <class P>
+template <class P, class KP>
 spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
                    bool do_lm) {
   const spr::Dims& d = m->d;
@@ -268,7 +268,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
     {
-      EpiQKV<P> e{};
+      EpiQKV<P, KP> e{};
       e.n_rows = n;
       e.H = d.H;
       e.Hkv = d.Hkv;
@@ -277,8 +277,8 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       e.dnorm = d.d;
       e.eps = d.eps;
       e.q = p.q();
-      e.kc = reinterpret_cast<E*>(p.kc(l));
-      e.vc = reinterpret_cast<E*>(p.vc(l));
+      e.kc = reinterpret_cast<typename KP::elem*>(p.kc(l));
+      e.vc = reinterpret_cast<typename KP::elem*>(p.vc(l));
       e.bt = p.bt();
       e.rope = p.rope();
       e.rows = sp;
@@ -301,7 +301,8 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       a.Rp = Rp;
       a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
       a.rows = sp;
-      st = d.hd == 128 ? launch_attention<P, 128>(m, a, max_splits) : launch_attention<P, 64>(m, a, max_splits);
+      st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a, max_splits)
+                       : launch_attention<P, KP, 64>(m, a, max_splits);
       if (st != SPR_OK) return st;
     }
     {
@@ -379,8 +380,9 @@ spr_status launch_projection(spr_model* m, int projection, int layer, int n) {
 
 spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
                        bool do_lm) {
-  return m->d.dtype == SPR_BF16 ? forward<BF16>(m, rs, tok_in, tok_out, logits, do_lm)
-                                : forward<F32>(m, rs, tok_in, tok_out, logits, do_lm);
+  if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, do_lm);
+  return m->d.kv_dtype == SPR_BF16 ? forward<BF16, BF16>(m, rs, tok_in, tok_out, logits, do_lm)
+                                   : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, do_lm);
 }
 
 spr_status check_model(const spr_model* m) {

@@ -12,7 +12,7 @@ from paper_2403_12900_amd.configs import ModelConfig
 
 def oracle_shape(m: ModelConfig) -> R.Shape:
     return R.Shape(m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff, m.vocab,
-                   m.rope_base, m.rms_eps, m.bf16)
+                   m.rope_base, m.rms_eps, m.bf16, kv_bf16=m.kv_is_bf16)
 
 
 def say(*a):
@@ -70,7 +70,9 @@ class DeviceRun:
         self.lens = lens
 
     def close(self):
+        import torch
         self.m.close()
+        torch.cuda.empty_cache()
 
 
 def compare_logits(dev: np.ndarray, ref: np.ndarray, dev_tok: int, abs_tol: float, rel_tol: float, tag: str):
@@ -109,7 +111,11 @@ def check_against_oracle(run: DeviceRun, w: R.Weights, prompts, stops, requests,
         steps = [s for s in steps if s in run.logits[i]]
         if not steps:
             continue
-        ref = R.teacher_forced_logits(w, prompts[i], run.tokens[i], steps)
+        every = max(1, w.shape.n_layers // 8)
+        ref = R.teacher_forced_logits(
+            w, prompts[i], run.tokens[i], steps,
+            progress=lambda l: say(f"  oracle request {i}: layer {l + 1}/{w.shape.n_layers}")
+            if (l + 1) % every == 0 else None)
         for r, s in enumerate(steps):
             mx, rel, near = compare_logits(run.logits[i][s], ref[r], run.tokens[i][s], abs_tol, rel_tol,
                                            f"request {i} step {s}")

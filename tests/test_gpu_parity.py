@@ -105,6 +105,10 @@ TOY_CASES = {
     "bf16_batch40_jt4": (
         ModelConfig(n_layers=1, d_model=64, n_heads=1, n_kv_heads=1, head_dim=64, d_ff=64, vocab=300),
         list(range(1, 41)), [3] * 40),
+    "bf16_weights_fp32_kv_gqa8": (
+        ModelConfig(n_layers=2, d_model=256, n_heads=8, n_kv_heads=1, head_dim=128, d_ff=344, vocab=500,
+                    kv_bf16=False),
+        [40, 3, 17, 90, 1], [5, 9, 2, 4, 6]),
     "bf16_long_context_splits": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=128, vocab=500),
         [700, 300], [20, 3]),
@@ -224,3 +228,44 @@ def test_llama2_7b_ragged_batch32_sampled():
     say("c3 sampled", st)
     assert st["rows"] == sum(len(v) for v in steps.values())
     run.close()
+
+
+# ------------------------------------------------------------------ the other full-size configurations
+
+def _sampled_full_size(key, n_requests, extra_steps=()):
+    cfg = CONFIGS[key]
+    wl = make_workload(cfg)
+    seq, stops = wl.seq_lens, wl.stop_lens
+    order = np.argsort(seq + stops)
+    sampled = [int(i) for i in order[:n_requests]]
+    steps = {}
+    for i in sampled:
+        L = int(stops[i])
+        steps[i] = sorted(({0, 1, 2, L // 2, L - 2, L - 1} | set(extra_steps)) & set(range(L)))
+    record = set().union(*steps.values())
+    say(f"{cfg.name}: sampled requests {sampled}, steps {steps}")
+    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops.tolist(), record=record)
+    assert run.active == R.active_schedule(stops.tolist())
+    assert [len(t) for t in run.tokens] == stops.tolist()
+    say(f"{cfg.name}: device decode done; oracle")
+    w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed, resident=False)
+    st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL, steps_of=lambda i: steps[i])
+    say(cfg.name, st)
+    assert st["rows"] == sum(len(v) for v in steps.values())
+    run.close()
+
+
+def test_llama2_7b_batch1_256_tokens():
+    """The latency case: one request, prompt 128, 256 generated tokens, checked at spread-out steps."""
+    _sampled_full_size("c2", 1, extra_steps=(64, 127, 200))
+
+
+def test_llama2_13b_ragged_batch64_sampled():
+    """13B shape, 64 ragged requests in 16-position KV pages; the two shortest requests are checked."""
+    _sampled_full_size("c4", 2)
+
+
+def test_llama2_70b_gqa_ragged_batch16_sampled():
+    """70B shape with grouped-query attention (8 query heads per KV head), ~138 GB of weights on one GPU;
+    the shortest request is checked against the oracle (which streams the weights layer by layer)."""
+    _sampled_full_size("c5", 1)
