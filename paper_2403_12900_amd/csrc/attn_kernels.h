@@ -2,7 +2,7 @@
 // (Section II-A: each new token attends to the cached keys and values of all
 // earlier tokens of its request, the directive prefix included).
 //
-// Work item = (KV split, row, KV head).  A workgroup of four waves walks the
+// Work item = (row, KV split, KV head).  A workgroup of four waves walks the
 // 16-position blocks of its split, wave w taking every fourth block.  Per
 // block, on MFMA:
 //   S[t][h]  = K_tile(16 x hd) . Q^T(hd x 16)      -- t = position, h = query
@@ -12,9 +12,10 @@
 //   log2e-scaled scores)
 //   O^T[e][h] += V^T_tile(hd x 16) . P(16 x 16)   -- P is the S accumulator
 //              re-used in place as the B operand: no shuffle, no LDS
-// The four waves are merged through LDS (log-sum-exp), and a split's result
-// either is final (written as the O-projection input) or goes to a partial
-// buffer merged by k_attn_merge.
+// The four waves are merged through LDS (log-sum-exp).  A row whose context
+// needs one split writes its output directly; otherwise each split writes a
+// partial (max, sum, unnormalised output) and k_attn_merge combines them.
+// The grid holds only (row, split) pairs with work.
 // bf16 keys are multiplied by q split into hi + lo bf16 parts, so the scores
 // carry fp32-level precision of q.
 #pragma once
@@ -33,12 +34,8 @@ struct AttnArgs {
   int n_rows, H, Hkv, G, mb, bps, Rp;
   float qscale;           // log2(e) / sqrt(hd)
   RowSlotPos rows;
+  int split_start[kRows + 1];  // first flat split index of each row; [n_rows] = total
 };
-
-__device__ __forceinline__ int attn_nsplit(int pos, int bps) {
-  const int nblk = (pos + 1 + 15) >> 4;
-  return (nblk + bps - 1) / bps;
-}
 
 // Four consecutive positions of one V^T row (one dimension), as loaded.
 template <class P>
@@ -130,12 +127,24 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   constexpr bool kBf16 = sizeof(E) == 2;
   constexpr int NF = Blk::NF;
   constexpr int NE = Blk::NE;
-  const int s = blockIdx.x, b = blockIdx.y, kvh = blockIdx.z;
+  // Flat grid over the (row, split) pairs that have work: find this
+  // work-group's row by binary search over the rows' first split index.
+  const int f = blockIdx.x, kvh = blockIdx.y;
+  int lo_r = 0, hi_r = a.n_rows - 1;
+  while (lo_r < hi_r) {  // first row whose splits end after f
+    const int mid = (lo_r + hi_r) >> 1;
+    if (a.split_start[mid + 1] <= f) {
+      lo_r = mid + 1;
+    } else {
+      hi_r = mid;
+    }
+  }
+  const int b = lo_r;
+  const int s = f - a.split_start[b];
+  const int nsplit = a.split_start[b + 1] - a.split_start[b];
   const int pos = a.rows.pos[b];
   const int ctx = pos + 1;
   const int nblk = (ctx + 15) >> 4;
-  const int nsplit = (nblk + a.bps - 1) / a.bps;
-  if (s >= nsplit) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane & 15, g = lane >> 4;
@@ -222,75 +231,82 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
       for (int r = 0; r < 4; ++r) sm[wave - 1][2 + 4 * e + r][lane] = O[e][r];
   }
   __syncthreads();
-  if (wave != 0) return;
-  // Wave 0 always holds at least one block (lo < nblk for s < nsplit), so M is
-  // finite; waves without blocks carry m = -inf and weigh 0.
-  float M = m_run;
-  for (int w = 0; w < 3; ++w) M = fmaxf(M, sm[w][0][lane]);
-  const float c0 = __builtin_amdgcn_exp2f(m_run - M);
-  float L = l_run * c0;
-#pragma unroll
-  for (int e = 0; e < NE; ++e)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) O[e][r] *= c0;
-  for (int w = 0; w < 3; ++w) {
-    const float cw = __builtin_amdgcn_exp2f(sm[w][0][lane] - M);
-    L += cw * sm[w][1][lane];
-#pragma unroll
-    for (int e = 0; e < NE; ++e)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) O[e][r] += cw * sm[w][2 + 4 * e + r][lane];
-  }
-  if (!hv) return;
   const int hq = kvh * a.G + h;
-  if (nsplit == 1) {
-    const float inv = 1.f / L;
-    typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
+  if (wave == 0) {
+    // Wave 0 always holds at least one block (lo < nblk for s < nsplit), so
+    // M is finite; waves without blocks carry m = -inf and weigh 0.
+    float M = m_run;
+    for (int w = 0; w < 3; ++w) M = fmaxf(M, sm[w][0][lane]);
+    const float c0 = __builtin_amdgcn_exp2f(m_run - M);
+    float L = l_run * c0;
 #pragma unroll
     for (int e = 0; e < NE; ++e)
-      store_act4<AP>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
-                     O[e][3] * inv);
-  } else {
-    float* pp = a.part + ((static_cast<size_t>(b) * a.H + hq) * kSplitsMax + s) * (HD + 4);
-    if (g == 0) {
-      pp[0] = M;
-      pp[1] = L;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) O[e][r] *= c0;
+    for (int w = 0; w < 3; ++w) {
+      const float cw = __builtin_amdgcn_exp2f(sm[w][0][lane] - M);
+      L += cw * sm[w][1][lane];
+#pragma unroll
+      for (int e = 0; e < NE; ++e)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) O[e][r] += cw * sm[w][2 + 4 * e + r][lane];
     }
+    if (hv) {
+      if (nsplit == 1) {
+        const float inv = 1.f / L;
+        typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
-    for (int e = 0; e < NE; ++e)
-      *reinterpret_cast<float4*>(pp + 4 + 16 * e + 4 * g) = make_float4(O[e][0], O[e][1], O[e][2], O[e][3]);
+        for (int e = 0; e < NE; ++e)
+          store_act4<AP>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
+                         O[e][3] * inv);
+      } else {
+        float* pp = a.part + ((static_cast<size_t>(b) * a.H + hq) * kSplitsMax + s) * (HD + 4);
+        if (g == 0) {
+          pp[0] = M;
+          pp[1] = L;
+        }
+#pragma unroll
+        for (int e = 0; e < NE; ++e)
+          *reinterpret_cast<float4*>(pp + 4 + 16 * e + 4 * g) = make_float4(O[e][0], O[e][1], O[e][2], O[e][3]);
+      }
+    }
   }
 }
 
-// Log-sum-exp merge of the KV splits of rows that needed more than one.  All
-// splits' statistics and values are loaded before any is combined.  P is the
-// activation format of the output.
-template <class P, int HD>
-__global__ __launch_bounds__(HD) void k_attn_merge(AttnArgs a) {
-  const int b = blockIdx.x, hq = blockIdx.y, dd = threadIdx.x;
-  const int nsplit = attn_nsplit(a.rows.pos[b], a.bps);
+// Log-sum-exp merge of the KV splits of one (row, KV head), for rows whose
+// context needed more than one split; all splits' statistics and values are
+// loaded before any is combined.  (A last-arriving split could merge instead
+// of a second launch, but the device-scope release that needs -- a write-back
+// of the XCD's L2 by every split -- measured ten times slower on MI355X.)
+template <class AP, int HD>
+__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
+  const int b = blockIdx.x, kvh = blockIdx.y;
+  const int nsplit = a.split_start[b + 1] - a.split_start[b];
   if (nsplit <= 1) return;
-  const float* pp = a.part + (static_cast<size_t>(b) * a.H + hq) * kSplitsMax * (HD + 4);
-  float m[kSplitsMax], l[kSplitsMax], o[kSplitsMax];
+  typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
+  for (int idx = threadIdx.x; idx < a.G * HD; idx += 256) {
+    const int hm = kvh * a.G + idx / HD, dd = idx % HD;
+    const float* pp = a.part + (static_cast<size_t>(b) * a.H + hm) * kSplitsMax * (HD + 4);
+    float m[kSplitsMax], l[kSplitsMax], o[kSplitsMax];
 #pragma unroll
-  for (int s = 0; s < kSplitsMax; ++s) {
-    const bool v = s < nsplit;
-    m[s] = v ? pp[s * (HD + 4)] : -INFINITY;
-    l[s] = v ? pp[s * (HD + 4) + 1] : 0.f;
-    o[s] = v ? pp[s * (HD + 4) + 4 + dd] : 0.f;
+    for (int t = 0; t < kSplitsMax; ++t) {
+      const bool v = t < nsplit;
+      m[t] = v ? pp[t * (HD + 4)] : -INFINITY;
+      l[t] = v ? pp[t * (HD + 4) + 1] : 0.f;
+      o[t] = v ? pp[t * (HD + 4) + 4 + dd] : 0.f;
+    }
+    float M = m[0];
+#pragma unroll
+    for (int t = 1; t < kSplitsMax; ++t) M = fmaxf(M, m[t]);
+    float L = 0.f, Ov = 0.f;
+#pragma unroll
+    for (int t = 0; t < kSplitsMax; ++t) {
+      const float c = __builtin_amdgcn_exp2f(m[t] - M);
+      L += c * l[t];
+      Ov += c * o[t];
+    }
+    act_store<AP>(act, a.Rp, b, hm * HD + dd, Ov / L);
   }
-  float M = m[0];
-#pragma unroll
-  for (int s = 1; s < kSplitsMax; ++s) M = fmaxf(M, m[s]);
-  float L = 0.f, O = 0.f;
-#pragma unroll
-  for (int s = 0; s < kSplitsMax; ++s) {
-    const float c = __builtin_amdgcn_exp2f(m[s] - M);
-    L += c * l[s];
-    O += c * o[s];
-  }
-  const int k = hq * HD + dd;
-  act_store<P>(static_cast<typename P::elem*>(a.act), a.Rp, b, k, O / L);
 }
 
 }  // namespace sprk

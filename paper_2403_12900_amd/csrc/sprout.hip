@@ -206,12 +206,11 @@ spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int K
 }
 
 template <class P, class KP, int HD>
-spr_status launch_attention(spr_model* m, const AttnArgs& a, int max_splits) {
-  dim3 grid(max_splits, a.n_rows, a.Hkv);
-  k_attn_decode<KP, P, HD><<<grid, 256, 0, m->st>>>(a);
+spr_status launch_attention(spr_model* m, const AttnArgs& a) {
+  k_attn_decode<KP, P, HD><<<dim3(a.split_start[a.n_rows], a.Hkv), 256, 0, m->st>>>(a);
   SPR_LAUNCHED(m, "k_attn_decode");
-  if (max_splits > 1) {
-    k_attn_merge<P, HD><<<dim3(a.n_rows, a.H), HD, 0, m->st>>>(a);
+  if (a.split_start[a.n_rows] > a.n_rows) {  // some row has more than one split
+    k_attn_merge<P, HD><<<dim3(a.n_rows, a.Hkv), 256, 0, m->st>>>(a);
     SPR_LAUNCHED(m, "k_attn_merge");
   }
   return SPR_OK;
@@ -263,7 +262,6 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
   bpw = bpw < 1 ? 1 : bpw > 4 ? 4 : bpw;
   if (ceil_div(max_blk, 4 * bpw) > kSplitsMax) bpw = ceil_div(ceil_div(max_blk, kSplitsMax), 4);
   const int bps = 4 * bpw;
-  const int max_splits = ceil_div(max_blk, bps);
 
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
@@ -301,8 +299,9 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       a.Rp = Rp;
       a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
       a.rows = sp;
-      st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a, max_splits)
-                       : launch_attention<P, KP, 64>(m, a, max_splits);
+      a.split_start[0] = 0;
+      for (int r = 0; r < n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, bps);
+      st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a) : launch_attention<P, KP, 64>(m, a);
       if (st != SPR_OK) return st;
     }
     {
