@@ -2,9 +2,9 @@
 // (Section II-A: each new token attends to the cached keys and values of all
 // earlier tokens of its request, the directive prefix included).
 //
-// Work item = (row, KV split, KV head).  A workgroup of four waves walks the
-// 16-position blocks of its split, wave w taking every fourth block.  Per
-// block, on MFMA:
+// Work item = (row, KV split, KV head).  A workgroup of four waves covers the
+// 16-position blocks of its split, each wave a contiguous run of bpw blocks.
+// Per block, on MFMA:
 //   S[t][h]  = K_tile(16 x hd) . Q^T(hd x 16)      -- t = position, h = query
 //              head of the KV group (G <= 16 columns used; grouped-query heads
 //              share the K/V tile they read once)
@@ -12,10 +12,11 @@
 //   log2e-scaled scores)
 //   O^T[e][h] += V^T_tile(hd x 16) . P(16 x 16)   -- P is the S accumulator
 //              re-used in place as the B operand: no shuffle, no LDS
-// The four waves are merged through LDS (log-sum-exp).  A row whose context
-// needs one split writes its output directly; otherwise each split writes a
-// partial (max, sum, unnormalised output) and k_attn_merge combines them.
-// The grid holds only (row, split) pairs with work.
+// The four waves are merged through LDS (log-sum-exp), each wave combining a
+// quarter of the head dimensions.  A row whose context needs one split writes
+// its output directly; otherwise each split writes a partial (max, sum,
+// unnormalised output) and k_attn_merge combines them.  The grid holds only
+// (row, split) pairs with work.
 // bf16 keys are multiplied by q split into hi + lo bf16 parts, so the scores
 // carry fp32-level precision of q.
 #pragma once
@@ -26,139 +27,152 @@ namespace sprk {
 
 struct AttnArgs {
   const float* q;         // [rows][H][hd], fp32
-  const void* kc;         // this layer's K blocks [block][Hkv][16 x hd in fragment order]
-  const void* vc;         // this layer's V blocks [block][Hkv][hd][16]
+  const void* kc;         // this layer's K blocks [block][Hkv][16 x hd, ktile_offset order]
+  const void* vc;         // this layer's V blocks [block][Hkv][16 x hd, vtile_offset order]
   const int32_t* bt;      // [slots][mb]
   void* act;              // output, K-block-major over H * hd
-  float* part;            // [rows][H][kSplitsMax][hd + 4]: m, l, -, -, o[hd]
-  int n_rows, H, Hkv, G, mb, bps, Rp;
+  float* part;            // [flat split][H][hd + 4]: m, l, -, -, o[hd]
+  int n_rows, H, Hkv, G, mb, bpw, Rp;
   float qscale;           // log2(e) / sqrt(hd)
   RowSlotPos rows;
   int split_start[kRows + 1];  // first flat split index of each row; [n_rows] = total
 };
 
-// Four consecutive positions of one V^T row (one dimension), as loaded.
-template <class P>
-struct VQuad;
-template <>
-struct VQuad<BF16> {
-  uint2 raw;
-  __device__ __forceinline__ void load(const uint16_t* v) {
-    typedef unsigned int u2v __attribute__((ext_vector_type(2)));
-    const u2v t = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(v));
-    raw = make_uint2(t.x, t.y);
-  }
-  // Positions past the context hold stale or never-written cache memory; they
-  // get probability 0, but 0 * NaN would still poison the sum, so zero them.
-  __device__ __forceinline__ void mask(int valid) {
-    raw.x &= valid >= 2 ? 0xFFFFFFFFu : valid == 1 ? 0xFFFFu : 0u;
-    raw.y &= valid >= 4 ? 0xFFFFFFFFu : valid == 3 ? 0xFFFFu : 0u;
-  }
-};
-template <>
-struct VQuad<F32> {
-  uint4 raw;
-  __device__ __forceinline__ void load(const float* v) { raw = load_weight<true>(reinterpret_cast<const uint4*>(v)); }
-  __device__ __forceinline__ void mask(int valid) {
-    raw.x = valid >= 1 ? raw.x : 0u;
-    raw.y = valid >= 2 ? raw.y : 0u;
-    raw.z = valid >= 3 ? raw.z : 0u;
-    raw.w = valid >= 4 ? raw.w : 0u;
-  }
-};
-
-// acc(16 dims x 16 heads) += V^T(16 dims x 16 positions) . P(16 positions x 16 heads).
-// bf16: the probabilities go in as hi + lo parts (two MFMAs).
-__device__ __forceinline__ f32x4_t mma_tok16(f32x4_t acc, const VQuad<BF16>& v, const float* p) {
-  const s16x4_t a = __builtin_bit_cast(s16x4_t, v.raw);
-  s16x4_t bh, bl;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const uint16_t h = f32_to_bf16_bits(p[r]);
-    bh[r] = static_cast<short>(h);
-    bl[r] = static_cast<short>(f32_to_bf16_bits(p[r] - bf16_bits_to_f32(h)));
-  }
-  acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, acc, 0, 0, 0);
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, acc, 0, 0, 0);
-}
-
-__device__ __forceinline__ f32x4_t mma_tok16(f32x4_t acc, const VQuad<F32>& v, const float* p) {
-  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.x), p[0], acc, 0, 0, 0);
-  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.y), p[1], acc, 0, 0, 0);
-  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.z), p[2], acc, 0, 0, 0);
-  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(v.raw.w), p[3], acc, 0, 0, 0);
-  return acc;
-}
-
-// K and V of one 16-position block of one KV head, in registers.  Each cached
-// byte is read once per step, so the loads are streaming (nontemporal).
+// K and V of one 16-position block of one KV head, in registers: NF K
+// operands and NV 16-byte V loads (two bf16 V^T operands or one fp32 operand
+// each, see vtile_offset).  Each cached byte is read once per step, so the
+// loads are streaming (nontemporal).
 template <class P, int HD>
 struct KVBlock {
   using E = typename P::elem;
-  static constexpr int NF = HD / P::kblk;  // K fragments (1 KiB each)
-  static constexpr int NE = HD / 16;       // V^T fragments, 16 dims each
+  static constexpr int NF = HD / P::kblk;
+  static constexpr int NV = HD * 16 * static_cast<int>(sizeof(E)) / 1024;
   uint4 kf[NF];
-  VQuad<P> vq[NE];
+  uint4 vf[NV];
 
   __device__ __forceinline__ void load(const E* kc, const E* vc, size_t tile, int lane) {
     const uint4* kt = reinterpret_cast<const uint4*>(kc + tile * 16 * HD) + lane;
+    const uint4* vt = reinterpret_cast<const uint4*>(vc + tile * 16 * HD) + lane;
 #pragma unroll
     for (int f = 0; f < NF; ++f) kf[f] = load_weight<true>(kt + f * 64);
-    const E* vt = vc + (tile * HD + (lane & 15)) * 16 + 4 * (lane >> 4);
 #pragma unroll
-    for (int e = 0; e < NE; ++e) vq[e].load(vt + e * 16 * 16);
+    for (int v = 0; v < NV; ++v) vf[v] = load_weight<true>(vt + v * 64);
+  }
+
+  // Positions past the context hold stale or never-written cache memory; they
+  // get probability 0, but 0 * NaN would still poison the sum, so zero them.
+  // `valid` = positions of this lane's four (4 g .. 4 g + 3) that are in context.
+  __device__ __forceinline__ void mask_v(int valid) {
+    if constexpr (sizeof(E) == 2) {
+      const uint32_t m01 = valid >= 2 ? 0xFFFFFFFFu : valid == 1 ? 0xFFFFu : 0u;
+      const uint32_t m23 = valid >= 4 ? 0xFFFFFFFFu : valid == 3 ? 0xFFFFu : 0u;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        vf[v].x &= m01;
+        vf[v].y &= m23;
+        vf[v].z &= m01;
+        vf[v].w &= m23;
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        vf[v].x = valid >= 1 ? vf[v].x : 0u;
+        vf[v].y = valid >= 2 ? vf[v].y : 0u;
+        vf[v].z = valid >= 3 ? vf[v].z : 0u;
+        vf[v].w = valid >= 4 ? vf[v].w : 0u;
+      }
+    }
+  }
+
+  // O[e] (16 dims x 16 heads) += V^T(16 dims x 16 positions) . P(16 positions
+  // x 16 heads), P given as this lane's four probabilities.  bf16: the
+  // probabilities go in as hi + lo parts (two MFMAs per operand).
+  __device__ __forceinline__ void pv(f32x4_t* O, const float* p) const {
+    if constexpr (sizeof(E) == 2) {
+      s16x4_t bh, bl;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint16_t h = f32_to_bf16_bits(p[r]);
+        bh[r] = static_cast<short>(h);
+        bl[r] = static_cast<short>(f32_to_bf16_bits(p[r] - bf16_bits_to_f32(h)));
+      }
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const s16x4_t a0 = __builtin_bit_cast(s16x4_t, make_uint2(vf[v].x, vf[v].y));
+        const s16x4_t a1 = __builtin_bit_cast(s16x4_t, make_uint2(vf[v].z, vf[v].w));
+        O[2 * v] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, bh, O[2 * v], 0, 0, 0);
+        O[2 * v] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, bl, O[2 * v], 0, 0, 0);
+        O[2 * v + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, bh, O[2 * v + 1], 0, 0, 0);
+        O[2 * v + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, bl, O[2 * v + 1], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        O[v] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vf[v].x), p[0], O[v], 0, 0, 0);
+        O[v] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vf[v].y), p[1], O[v], 0, 0, 0);
+        O[v] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vf[v].z), p[2], O[v], 0, 0, 0);
+        O[v] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vf[v].w), p[3], O[v], 0, 0, 0);
+      }
+    }
   }
 };
 
 // P is the KV-cache storage format (it also sets the MFMA operand type of q
 // and of the probabilities); AP is the format of the output activation.
-// Work-group (split s, row b, KV head): blocks [s * bps, min(nblk, (s + 1) *
-// bps)); wave w takes the contiguous run of bps / 4 blocks starting at
-// w * bps / 4.  A wave walks its blocks one at a time -- load K and V, scores,
-// online-softmax update, P V -- with few registers, so that several waves per
-// SIMD hide each other's memory latency (measured faster on MI355X than
-// keeping two blocks in flight per wave at lower occupancy).  Branch
-// conditions are wave-uniform; the partial last block of the context is
-// masked by selects.
+// Work-group (flat split f, KV head): row b and split s of f; blocks [s * 4
+// bpw, min(nblk, (s + 1) * 4 bpw)); wave w takes the run of bpw blocks from
+// s * 4 bpw + w * bpw.  A wave walks its blocks one at a time -- load K and
+// V, scores, online-softmax update, P V -- with few registers, so that
+// several waves per SIMD hide each other's memory latency (measured faster on
+// MI355X than keeping two blocks in flight per wave at lower occupancy); the
+// block ids of its run come in one vector load up front, so each block costs
+// one memory round trip.  Branch conditions are wave-uniform; the partial
+// last block of the context is masked by selects.
 template <class P, class AP, int HD>
 __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   using E = typename P::elem;
   using Blk = KVBlock<P, HD>;
   constexpr bool kBf16 = sizeof(E) == 2;
   constexpr int NF = Blk::NF;
-  constexpr int NE = Blk::NE;
-  // Flat grid over the (row, split) pairs that have work: find this
-  // work-group's row by binary search over the rows' first split index.
+  constexpr int NE = HD / 16;     // output operands (16 dims each)
+  constexpr int EPW = NE / 4;     // output operands each wave merges and stores
   const int f = blockIdx.x, kvh = blockIdx.y;
-  int lo_r = 0, hi_r = a.n_rows - 1;
-  while (lo_r < hi_r) {  // first row whose splits end after f
-    const int mid = (lo_r + hi_r) >> 1;
-    if (a.split_start[mid + 1] <= f) {
-      lo_r = mid + 1;
-    } else {
-      hi_r = mid;
-    }
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // Row of this work-group = number of rows whose splits all precede f (the
+  // split starts increase), counted with one ballot per 64 rows.
+  int b = 0;
+  for (int r0 = 0; r0 < a.n_rows - 1; r0 += 64) {
+    const int r = r0 + lane;
+    b += __popcll(__ballot(r < a.n_rows - 1 && a.split_start[r + 1] <= f));
   }
-  const int b = lo_r;
+  b = __builtin_amdgcn_readfirstlane(b);
   const int s = f - a.split_start[b];
   const int nsplit = a.split_start[b + 1] - a.split_start[b];
   const int pos = a.rows.pos[b];
   const int ctx = pos + 1;
   const int nblk = (ctx + 15) >> 4;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int h = lane & 15, g = lane >> 4;
   const bool hv = h < a.G;
-  const int bpw = a.bps / 4;
-  const int lo = min(nblk, s * a.bps + wave * bpw), hi = min(nblk, s * a.bps + (wave + 1) * bpw);
+  const int bpw = a.bpw;
+  const int lo = min(nblk, (4 * s + wave) * bpw), hi = min(nblk, (4 * s + wave + 1) * bpw);
   const int32_t* btrow = a.bt + static_cast<size_t>(a.rows.slot[b]) * a.mb;
+  int ids = lo + lane < hi ? btrow[lo + lane] : 0;  // block ids of the next 64 blocks of the run
 
   // Q^T operand (hi and lo parts for bf16), scaled so scores are in log2
   // units; fragment c, lane h + 16 g holds dims c * kblk + g * per16 + j,
   // matching the K tile order.
+  // Lanes of padding columns (h >= G) read head kvh * G's q (a valid
+  // address, so the loads are unconditional and vectorised) and zero it.
   uint4 qh[NF], ql[NF];
   {
     const float* qp = a.q + (static_cast<size_t>(b) * a.H + kvh * a.G + (hv ? h : 0)) * HD + g * P::per16;
+    float4 qv[NF][P::per16 / 4];
+#pragma unroll
+    for (int c = 0; c < NF; ++c)
+#pragma unroll
+      for (int j4 = 0; j4 < P::per16 / 4; ++j4) qv[c][j4] = *reinterpret_cast<const float4*>(qp + c * P::kblk + 4 * j4);
+    const float qs = hv ? a.qscale : 0.f;
 #pragma unroll
     for (int c = 0; c < NF; ++c) {
       union {
@@ -167,7 +181,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
       } vh, vl;
 #pragma unroll
       for (int j = 0; j < P::per16; ++j) {
-        const float v = hv ? qp[c * P::kblk + j] * a.qscale : 0.f;
+        const float4 t = qv[c][j / 4];
+        const float v = (j % 4 == 0 ? t.x : j % 4 == 1 ? t.y : j % 4 == 2 ? t.z : t.w) * qs;
         vh.e[j] = P::from_f32(v);
         vl.e[j] = P::from_f32(v - P::to_f32(vh.e[j]));
       }
@@ -184,20 +199,21 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   const E* vc = static_cast<const E*>(a.vc);
 
   for (int i = lo; i < hi; ++i) {
+    const int k = i - lo;
+    if ((k & 63) == 0 && k != 0) ids = i + lane < hi ? btrow[i + lane] : 0;
     Blk B;
-    B.load(kc, vc, static_cast<size_t>(btrow[i]) * a.Hkv + kvh, lane);
+    B.load(kc, vc, static_cast<size_t>(__builtin_amdgcn_readlane(ids, k & 63)) * a.Hkv + kvh, lane);
     f32x4_t S = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      S = P::mma(S, B.kf[f], qh[f]);
-      if constexpr (kBf16) S = P::mma(S, B.kf[f], ql[f]);
+    for (int c = 0; c < NF; ++c) {
+      S = P::mma(S, B.kf[c], qh[c]);
+      if constexpr (kBf16) S = P::mma(S, B.kf[c], ql[c]);
     }
     if (i == nblk - 1) {  // the block holding the context's last position
       const int valid = ctx - (i * 16 + 4 * g);
 #pragma unroll
       for (int r = 0; r < 4; ++r) S[r] = r < valid ? S[r] : -INFINITY;
-#pragma unroll
-      for (int e = 0; e < NE; ++e) B.vq[e].mask(valid);
+      B.mask_v(valid);
     }
     float mb = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
     mb = fmaxf(mb, __shfl_xor(mb, 16));
@@ -208,104 +224,122 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(S[r] - m_new);
     l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-    m_run = m_new;
+    // O is still zero at the first block; later, rescale only if some
+    // column's running maximum moved (alpha == 1 elsewhere).
+    if (i != lo && __ballot(m_new != m_run) != 0) {
 #pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      O[e][0] *= alpha;
-      O[e][1] *= alpha;
-      O[e][2] *= alpha;
-      O[e][3] *= alpha;
-      O[e] = mma_tok16(O[e], B.vq[e], p);
+      for (int e = 0; e < NE; ++e) {
+        O[e][0] *= alpha;
+        O[e][1] *= alpha;
+        O[e][2] *= alpha;
+        O[e][3] *= alpha;
+      }
     }
+    m_run = m_new;
+    B.pv(O, p);
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
 
-  __shared__ float sm[3][2 + 4 * NE][64];
-  if (wave > 0) {
-    sm[wave - 1][0][lane] = m_run;
-    sm[wave - 1][1][lane] = l_run;
+  // Log-sum-exp merge of the four waves; wave w combines and stores output
+  // operands [w * EPW, (w + 1) * EPW).  Wave 0 always holds at least one
+  // block (its run starts the split), so M is finite; waves without blocks
+  // carry m = -inf and weigh 0.
+  __shared__ f32x4_t so[4][NE][64];
+  __shared__ float2 sml[4][64];
+  sml[wave][lane] = make_float2(m_run, l_run);
 #pragma unroll
-    for (int e = 0; e < NE; ++e)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sm[wave - 1][2 + 4 * e + r][lane] = O[e][r];
-  }
+  for (int e = 0; e < NE; ++e) so[wave][e][lane] = O[e];
   __syncthreads();
+  float2 ml[4];
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    ml[w] = sml[w][lane];
+    M = fmaxf(M, ml[w].x);
+  }
+  float cw[4], L = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    cw[w] = __builtin_amdgcn_exp2f(ml[w].x - M);
+    L += cw[w] * ml[w].y;
+  }
+  f32x4_t R[EPW];
+#pragma unroll
+  for (int k = 0; k < EPW; ++k) {
+    R[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const f32x4_t o = so[w][wave * EPW + k][lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) R[k][r] += cw[w] * o[r];
+    }
+  }
+  if (!hv) return;
   const int hq = kvh * a.G + h;
-  if (wave == 0) {
-    // Wave 0 always holds at least one block (lo < nblk for s < nsplit), so
-    // M is finite; waves without blocks carry m = -inf and weigh 0.
-    float M = m_run;
-    for (int w = 0; w < 3; ++w) M = fmaxf(M, sm[w][0][lane]);
-    const float c0 = __builtin_amdgcn_exp2f(m_run - M);
-    float L = l_run * c0;
+  if (nsplit == 1) {
+    const float inv = 1.f / L;
+    typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
-    for (int e = 0; e < NE; ++e)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) O[e][r] *= c0;
-    for (int w = 0; w < 3; ++w) {
-      const float cw = __builtin_amdgcn_exp2f(sm[w][0][lane] - M);
-      L += cw * sm[w][1][lane];
-#pragma unroll
-      for (int e = 0; e < NE; ++e)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) O[e][r] += cw * sm[w][2 + 4 * e + r][lane];
+    for (int k = 0; k < EPW; ++k)
+      store_act4<AP>(act, a.Rp, b, hq * HD + 16 * (wave * EPW + k) + 4 * g, R[k][0] * inv, R[k][1] * inv,
+                     R[k][2] * inv, R[k][3] * inv);
+  } else {
+    float* pp = a.part + (static_cast<size_t>(f) * a.H + hq) * (HD + 4);
+    if (wave == 0 && g == 0) {
+      pp[0] = M;
+      pp[1] = L;
     }
-    if (hv) {
-      if (nsplit == 1) {
-        const float inv = 1.f / L;
-        typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
-        for (int e = 0; e < NE; ++e)
-          store_act4<AP>(act, a.Rp, b, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv, O[e][2] * inv,
-                         O[e][3] * inv);
-      } else {
-        float* pp = a.part + ((static_cast<size_t>(b) * a.H + hq) * kSplitsMax + s) * (HD + 4);
-        if (g == 0) {
-          pp[0] = M;
-          pp[1] = L;
-        }
-#pragma unroll
-        for (int e = 0; e < NE; ++e)
-          *reinterpret_cast<float4*>(pp + 4 + 16 * e + 4 * g) = make_float4(O[e][0], O[e][1], O[e][2], O[e][3]);
-      }
-    }
+    for (int k = 0; k < EPW; ++k)
+      *reinterpret_cast<float4*>(pp + 4 + 16 * (wave * EPW + k) + 4 * g) = make_float4(R[k][0], R[k][1], R[k][2], R[k][3]);
   }
 }
 
 // Log-sum-exp merge of the KV splits of one (row, KV head), for rows whose
-// context needed more than one split; all splits' statistics and values are
-// loaded before any is combined.  (A last-arriving split could merge instead
-// of a second launch, but the device-scope release that needs -- a write-back
-// of the XCD's L2 by every split -- measured ten times slower on MI355X.)
+// context needed more than one split.  Splits are taken kChunk at a time, all
+// of a chunk's loads issued before any is combined (indexes past the last
+// split re-read it and are then ignored).  (A last-arriving split could merge
+// instead of a second launch, but the device-scope release that needs -- a
+// write-back of the XCD's L2 by every split -- measured ten times slower on
+// MI355X.)
 template <class AP, int HD>
 __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
+  constexpr int kChunk = 32;
   const int b = blockIdx.x, kvh = blockIdx.y;
-  const int nsplit = a.split_start[b + 1] - a.split_start[b];
-  if (nsplit <= 1) return;
+  const int f0 = a.split_start[b];
+  const int ns = a.split_start[b + 1] - f0;
+  if (ns <= 1) return;
   typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
+  const size_t stride = static_cast<size_t>(a.H) * (HD + 4);
   for (int idx = threadIdx.x; idx < a.G * HD; idx += 256) {
-    const int hm = kvh * a.G + idx / HD, dd = idx % HD;
-    const float* pp = a.part + (static_cast<size_t>(b) * a.H + hm) * kSplitsMax * (HD + 4);
-    float m[kSplitsMax], l[kSplitsMax], o[kSplitsMax];
+    const int hq = kvh * a.G + idx / HD, dd = idx % HD;
+    const float* pp = a.part + (static_cast<size_t>(f0) * a.H + hq) * (HD + 4);
+    float M = -INFINITY, L = 0.f, Ov = 0.f;
+    for (int t0 = 0; t0 < ns; t0 += kChunk) {
+      float m[kChunk], l[kChunk], o[kChunk];
 #pragma unroll
-    for (int t = 0; t < kSplitsMax; ++t) {
-      const bool v = t < nsplit;
-      m[t] = v ? pp[t * (HD + 4)] : -INFINITY;
-      l[t] = v ? pp[t * (HD + 4) + 1] : 0.f;
-      o[t] = v ? pp[t * (HD + 4) + 4 + dd] : 0.f;
+      for (int k = 0; k < kChunk; ++k) {
+        const float* pt = pp + static_cast<size_t>(min(t0 + k, ns - 1)) * stride;
+        m[k] = pt[0];
+        l[k] = pt[1];
+        o[k] = pt[4 + dd];
+      }
+      float Mn = M;
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k) Mn = t0 + k < ns ? fmaxf(Mn, m[k]) : Mn;
+      const float sc = __builtin_amdgcn_exp2f(M - Mn);  // 0 while M = -inf
+      L *= sc;
+      Ov *= sc;
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k) {
+        const float c = t0 + k < ns ? __builtin_amdgcn_exp2f(m[k] - Mn) : 0.f;
+        L += c * l[k];
+        Ov += c * o[k];
+      }
+      M = Mn;
     }
-    float M = m[0];
-#pragma unroll
-    for (int t = 1; t < kSplitsMax; ++t) M = fmaxf(M, m[t]);
-    float L = 0.f, Ov = 0.f;
-#pragma unroll
-    for (int t = 0; t < kSplitsMax; ++t) {
-      const float c = __builtin_amdgcn_exp2f(m[t] - M);
-      L += c * l[t];
-      Ov += c * o[t];
-    }
-    act_store<AP>(act, a.Rp, b, hm * HD + dd, Ov / L);
+    act_store<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
   }
 }
 

@@ -110,6 +110,23 @@ __device__ __forceinline__ int ktile_offset(int t, int dd) {
   return ((dd / P::kblk) * 64 + ((dd % P::kblk) / P::per16) * 16 + t) * P::per16 + dd % P::per16;
 }
 
+// A V tile (16 positions x head_dim) is stored transposed, as the A operand
+// of O^T += V^T . P: in the operand for dims [16 e, 16 e + 16), lane r + 16 g
+// holds dim 16 e + r at positions 4 g .. 4 g + 3.  For bf16 the 8-byte
+// pieces of operands 2 c and 2 c + 1 of one lane are adjacent, so a lane
+// fetches both with one 16-byte load; for fp32 a lane's 16 bytes are one
+// operand.  Either way lane l's bytes of load v sit at byte (v * 64 + l) * 16
+// of the tile, and every wave load reads 1 KiB of consecutive bytes.
+template <class P>
+__device__ __forceinline__ int vtile_offset(int t, int dd) {
+  const int r = dd & 15, g = t >> 2, i = t & 3;
+  if constexpr (P::per16 == 8) {
+    return ((((dd >> 5) * 4 + g) * 16 + r) * 2 + ((dd >> 4) & 1)) * 4 + i;
+  } else {
+    return (((dd >> 4) * 4 + g) * 16 + r) * 4 + i;
+  }
+}
+
 template <class P>
 __device__ __forceinline__ void act_store(typename P::elem* act, int Rp, int b, int k, float v) {
   typename P::elem hi, lo;

@@ -29,7 +29,6 @@
 namespace sprk {
 
 constexpr int kRows = 128;      // token rows per pass
-constexpr int kSplitsMax = 16;  // decode-attention KV splits per (row, head)
 
 struct RowSlotPos {
   int slot[kRows];
@@ -224,9 +223,9 @@ __device__ __forceinline__ void store_act4(typename P::elem* act, int Rp, int b,
 // QKV projection -> RMSNorm scale -> RoPE on q and k -> q to the attention
 // input, k and v appended to the paged KV cache at the row's position.
 // Per (block, KV head) the K tile is 16 positions x head_dim in MFMA fragment
-// order (ktile_offset); V is stored transposed, [head_dim][16 positions], so
-// the attention kernel reads 4 consecutive positions of one dimension as one
-// MFMA operand.
+// order (ktile_offset) and the V tile is transposed into the operand order of
+// the P V product (vtile_offset), so the attention kernel reads both with
+// 16-byte loads straight into MFMA operands.
 template <class P, class KP = P>
 struct EpiQKV {
   static constexpr bool kNorm = true;
@@ -276,11 +275,11 @@ struct EpiQKV {
         dst[3] = KP::from_f32(v3);
       } else {
         const int m = n0 - qr - kr, kvh = m / hd, dd = m % hd;
-        typename KP::elem* dst = vc + ((static_cast<size_t>(blk) * Hkv + kvh) * hd + dd) * 16 + off;
-        dst[0] = KP::from_f32(v0);
-        dst[16] = KP::from_f32(v1);
-        dst[32] = KP::from_f32(v2);
-        dst[48] = KP::from_f32(v3);
+        typename KP::elem* dst = vc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd;
+        dst[vtile_offset<KP>(off, dd)] = KP::from_f32(v0);
+        dst[vtile_offset<KP>(off, dd + 1)] = KP::from_f32(v1);
+        dst[vtile_offset<KP>(off, dd + 2)] = KP::from_f32(v2);
+        dst[vtile_offset<KP>(off, dd + 3)] = KP::from_f32(v3);
       }
     }
   }

@@ -106,7 +106,7 @@ Layout layout(const Dims& d) {
   l.off_act0 = take(l.act_bytes);
   l.off_act1 = take(l.act_bytes);
   l.off_q = take(static_cast<size_t>(kMaxRows) * d.H * d.hd * sizeof(float));
-  l.off_part = take(static_cast<size_t>(kMaxRows) * d.H * kMaxSplits * (d.hd + 4) * sizeof(float));
+  l.off_part = take(static_cast<size_t>(kMaxSplits) * d.H * (d.hd + 4) * sizeof(float));
   l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
   l.total = off;
   return l;

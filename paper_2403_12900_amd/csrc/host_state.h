@@ -15,7 +15,7 @@ namespace spr {
 
 constexpr int kKvBlock = 16;     // positions per KV block
 constexpr int kMaxRows = 128;    // token rows per forward pass (prefill chunk)
-constexpr int kMaxSplits = 16;   // KV splits per (row, head) in decode attention
+constexpr int kMaxSplits = 2048; // KV splits over all rows of one pass (decode attention)
 constexpr int kFragBytes = 1024; // one MFMA operand fragment: 64 lanes x 16 bytes
 
 struct Dims {

@@ -248,20 +248,20 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     SPR_LAUNCHED(m, "k_embed");
   }
 
-  // KV splits: a work-group covers bps blocks of one (row, KV head), 4 waves
-  // of bps / 4 blocks each.  Waves get 1..4 blocks so that there are about
-  // 4096 of them (16 per CU) whenever the context allows, and at most
-  // kSplitsMax splits per (row, head).
-  int total_blk = 0, max_blk = 0;
-  for (int r = 0; r < n; ++r) {
-    const int nb = (rs.pos[r] + 1 + 15) / 16;
-    total_blk += nb;
-    if (nb > max_blk) max_blk = nb;
-  }
+  // KV splits: a work-group covers 4 * bpw blocks of one (row, KV head), a
+  // run of bpw blocks per wave.  bpw stays 1 until the pass has more blocks
+  // than about 4096 waves (16 per CU, the kernel's occupancy) take at once,
+  // and grows further only while the splits exceed the partial buffer.
+  int total_blk = 0;
+  for (int r = 0; r < n; ++r) total_blk += (rs.pos[r] + 1 + 15) / 16;
   int bpw = ceil_div(total_blk * d.Hkv, 4096);
-  bpw = bpw < 1 ? 1 : bpw > 4 ? 4 : bpw;
-  if (ceil_div(max_blk, 4 * bpw) > kSplitsMax) bpw = ceil_div(ceil_div(max_blk, kSplitsMax), 4);
-  const int bps = 4 * bpw;
+  if (bpw < 1) bpw = 1;
+  auto count_splits = [&](int w) {
+    int t = 0;
+    for (int r = 0; r < n; ++r) t += ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * w);
+    return t;
+  };
+  while (count_splits(bpw) > spr::kMaxSplits) ++bpw;
 
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
@@ -295,12 +295,12 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       a.Hkv = d.Hkv;
       a.G = d.G;
       a.mb = d.mb;
-      a.bps = bps;
+      a.bpw = bpw;
       a.Rp = Rp;
       a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
       a.rows = sp;
       a.split_start[0] = 0;
-      for (int r = 0; r < n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, bps);
+      for (int r = 0; r < n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw);
       st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a) : launch_attention<P, KP, 64>(m, a);
       if (st != SPR_OK) return st;
     }
