@@ -162,45 +162,45 @@ struct RowSet {
   int tok[kRows];
 };
 
-// Launch shape of a projection (measured on MI355X): projections with many
-// 16-row tiles use 4-wave work-groups, two tiles per work-group once more
-// than 8 rows share each activation fragment; narrow projections (fewer than
-// 512 tiles, e.g. the O and down projections) use one tile per work-group
-// and more waves, so every CU streams its tile with enough loads in flight.
-// Waves per work-group of a narrow projection; wider row sets need the
-// registers of fewer waves.
-template <int JT>
-constexpr int kNarrowWaves = JT == 1 ? 16 : JT <= 4 ? 8 : 4;
+// Launch shape of a projection, from sweeps over the 7B projection shapes on
+// MI355X at 1..32 rows:
+//   * wide projections (>= 1024 16-row tiles: gate/up, LM head) at up to 32
+//     rows: one-wave work-groups, each streaming two whole tiles over the
+//     full K -- long contiguous streams and no cross-wave reduction;
+//   * projections of 512..1023 tiles (QKV) at 17..64 rows: four waves split
+//     K for two tiles, so each activation fragment feeds two weight fragments;
+//   * everything else: four waves split K for one tile.
+template <class P, int JT, class Epi>
+void launch_gemm_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi) {
+  const int Rp = 16 * JT, n = epi.n_rows;
+  if constexpr (JT <= 2) {
+    if (NT >= 1024 && NT % 2 == 0) {
+      k_stream_gemm<P, JT, 1, Epi, 2, JT == 1 ? 8 : 4, true><<<NT / 2, 64, 0, st>>>(w, x, KB, Rp, n, epi);
+      return;
+    }
+  }
+  if constexpr (JT >= 2 && JT <= 4) {
+    if (NT >= 512 && NT % 2 == 0) {
+      k_stream_gemm<P, JT, 4, Epi, 2, StreamDepth<2 * JT * P::parts>::value, true><<<NT / 2, 256, 0, st>>>(
+          w, x, KB, Rp, n, epi);
+      return;
+    }
+  }
+  k_stream_gemm<P, JT, 4, Epi, 1, StreamDepth<JT * P::parts>::value, true><<<NT, 256, 0, st>>>(w, x, KB, Rp, n, epi);
+}
 
 template <class P, class Epi>
 spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int KB, int JT, const Epi& epi) {
   const uint4* w = reinterpret_cast<const uint4*>(W);
   const uint4* x = reinterpret_cast<const uint4*>(X);
-  const int Rp = 16 * JT;
-  const int n = epi.n_rows;
-  const bool narrow = NT < 512;
-  const bool pair = !narrow && (n > 8 || JT >= 2) && NT % 2 == 0 && JT <= 4;
-#define SPR_GEMM_CASE(JTV)                                                                               \
-  case JTV:                                                                                              \
-    if (narrow)                                                                                          \
-      k_stream_gemm<P, JTV, kNarrowWaves<JTV>, Epi, 1, StreamDepth<JTV * P::parts>::value, true>        \
-          <<<NT, kNarrowWaves<JTV> * 64, 0, m->st>>>(w, x, KB, Rp, n, epi);                              \
-    else if (pair)                                                                                       \
-      k_stream_gemm<P, JTV, 4, Epi, 2, StreamDepth<2 * JTV * P::parts>::value, true>                    \
-          <<<NT / 2, 256, 0, m->st>>>(w, x, KB, Rp, n, epi);                                             \
-    else                                                                                                 \
-      k_stream_gemm<P, JTV, 4, Epi, 1, StreamDepth<JTV * P::parts>::value, true>                        \
-          <<<NT, 256, 0, m->st>>>(w, x, KB, Rp, n, epi);                                                 \
-    break;
   switch (JT) {
-    SPR_GEMM_CASE(1)
-    SPR_GEMM_CASE(2)
-    SPR_GEMM_CASE(4)
-    SPR_GEMM_CASE(8)
+    case 1: launch_gemm_shape<P, 1>(m->st, NT, w, x, KB, epi); break;
+    case 2: launch_gemm_shape<P, 2>(m->st, NT, w, x, KB, epi); break;
+    case 4: launch_gemm_shape<P, 4>(m->st, NT, w, x, KB, epi); break;
+    case 8: launch_gemm_shape<P, 8>(m->st, NT, w, x, KB, epi); break;
     default:
       return fail(SPR_ERR_INVALID_ARG, "internal: unsupported row-tile count");
   }
-#undef SPR_GEMM_CASE
   SPR_LAUNCHED(m, "k_stream_gemm");
   return SPR_OK;
 }
