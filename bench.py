@@ -61,6 +61,90 @@ def measured_traffic(bytes_per_launch: float):
         return None
 
 
+PMC_COPY_BYTES = 256 << 20     # calibration copy of --traffic-probe
+
+
+def traffic_probe():
+    """Launches exactly what the roofline line times -- the gate/up projection at
+    8 rows, rotating through the 32 layers -- plus a plain device copy of known
+    size, for two rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE)."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    m = CONFIGS["c3"].model
+    torch.cuda.set_device(0)
+    model = DecodeModel(m, CONFIGS["c3"].weight_seed, max_slots=8, max_ctx=64, kv_blocks=32)
+    us = model.time_projection("gate_up", 8, 64)
+    log(f"traffic probe: 64 gate/up launches, {us:.2f} us each")
+    model.close()
+    x = torch.ones(PMC_COPY_BYTES, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(4):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    log(f"traffic probe: 4 device copies of {PMC_COPY_BYTES} bytes")
+
+
+def _pmc_rows(path: str, counter: str):
+    """(kernel name, value) per dispatch from a rocprofv3 counter_collection.csv."""
+    import csv
+    out = []
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r.get("Counter_Name") == counter:
+                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def traffic_summary(fetch_csv: str, write_csv: str) -> None:
+    """Writes the committed PMC summary that measured_traffic() reads."""
+    import re
+    import statistics
+
+    def norm(name):
+        return re.sub(r"\(.*", "", name).replace("sprk::", "").replace("void ", "").strip()
+
+    res = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = _pmc_rows(path, counter)
+        k = [v for n, v in rows if norm(n) == DOMINANT]
+        c = sorted((v for n, v in rows if "copy" in n.lower()), reverse=True)[:4]
+        if not k or len(c) < 4:
+            raise SystemExit(f"{path}: {len(k)} dispatches of {DOMINANT}, {len(c)} copies")
+        res[counter] = (statistics.mean(k), len(k), statistics.mean(c))
+    m_fetch, n_fetch, c_fetch = res["FETCH_SIZE"]
+    m_write, n_write, c_write = res["WRITE_SIZE"]
+    true_kib = PMC_COPY_BYTES / 1024.0
+    s_fetch, s_write = true_kib / c_fetch, true_kib / c_write
+    fetch_b = m_fetch * s_fetch * 1024.0
+    write_b = m_write * s_write * 1024.0
+    with open(TRAFFIC_PROFILE, "w") as fh:
+        fh.write(f"""# rocprofv3 PMC summary: HBM traffic of {DOMINANT}
+# (gate/up projection with SwiGLU, Llama-2-7B shape, 8 rows; each launch streams one layer's
+# 180.4 MB gate/up matrix, rotating through all 32 layers).
+# Commands (one MI355X; the repository at /root/repo; `cd /tmp && export TMPDIR=/tmp` first):
+#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d /tmp/pmc_fetch -o probe -- python3 /root/repo/bench.py --traffic-probe
+#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d /tmp/pmc_write -o probe -- python3 /root/repo/bench.py --traffic-probe
+#   python3 /root/repo/bench.py --traffic-summary /tmp/pmc_fetch/probe_counter_collection.csv /tmp/pmc_write/probe_counter_collection.csv
+# Each counter (KiB per dispatch) is scaled by the ratio true/measured of the same counter on a
+# plain device copy of {PMC_COPY_BYTES} bytes (reads and writes that many bytes).
+kernel = {DOMINANT}
+dispatches_fetch = {n_fetch}
+dispatches_write = {n_write}
+fetch_kib_per_dispatch = {m_fetch:.1f}
+write_kib_per_dispatch = {m_write:.1f}
+copy_fetch_kib = {c_fetch:.1f}
+copy_write_kib = {c_write:.1f}
+fetch_scale = {s_fetch:.4f}
+write_scale = {s_write:.4f}
+hbm_fetch_bytes_per_launch = {fetch_b:.0f}
+hbm_write_bytes_per_launch = {write_b:.0f}
+hbm_bytes_per_launch = {fetch_b + write_b:.0f}
+kernel_source_hash = {kernel_source_hash()}
+""")
+    print(open(TRAFFIC_PROFILE).read())
+
+
 def cpu_baseline(cfg, wl, seconds: float):
     """The CPU oracle's KV-cache decode step on the same workload, bounded sample."""
     import numpy as np
@@ -107,7 +191,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="only launch the dominant kernel and a calibration copy (for rocprofv3 --pmc)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the PMC traffic summary from two rocprofv3 counter_collection.csv files")
     args = ap.parse_args()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
+    if args.traffic_probe:
+        traffic_probe()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the decode path runs one model "
               "replica per GPU with no exchange between GPUs, and this build has no multi-GPU mode.",
