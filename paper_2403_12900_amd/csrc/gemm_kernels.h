@@ -112,6 +112,14 @@ __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restr
     xoff[j] = (b < n_rows ? b : 0) * 4 + (lane >> 4);
   }
   const size_t xpart = static_cast<size_t>(Rp) * 4;  // uint4 per (K-block, part)
+  // Operands the epilogue reads from memory (residual, rotary table, block
+  // table) are fetched now, by the wave that runs the epilogue, so their
+  // latency hides under the weight stream instead of ending the kernel.
+  typename Epi::Pre pre[RT];
+  if (wave == 0) {
+#pragma unroll
+    for (int t = 0; t < RT; ++t) pre[t] = epi.template prefetch<JT>(nt0 + t, lane);
+  }
 
   auto load = [&](Stage& st, int kb) {
 #pragma unroll
@@ -207,7 +215,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restr
     }
   }
 #pragma unroll
-  for (int t = 0; t < RT; ++t) epi.template apply<JT>(nt0 + t, acc[t], ssq, lane);
+  for (int t = 0; t < RT; ++t) epi.template apply<JT>(nt0 + t, acc[t], ssq, lane, pre[t]);
 }
 
 // Stores four consecutive features n0..n0+3 of row b into an activation buffer.
@@ -238,8 +246,34 @@ struct EpiQKV {
   const float2* rope;           // [positions][hd / 2] (cos, sin)
   RowSlotPos rows;
 
+  // Per row tile of a lane: the rotary (cos, sin) pairs of its four features
+  // (q and k rows) and the KV block its position falls in (k and v rows).
+  // Lanes of rows past n_rows fetch row 0's.
+  struct Pre {
+    float4 cs[kRows / 16];
+    int blk[kRows / 16];
+  };
   template <int JT>
-  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane) const {
+  __device__ __forceinline__ Pre prefetch(int nt, int lane) const {
+    Pre pr;
+    const int n0 = 16 * nt + 4 * (lane >> 4);
+    const int qr = H * hd, kr = Hkv * hd;
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+      const int b = 16 * j + (lane & 15);
+      const int bb = b < n_rows ? b : 0;
+      const int p = rows.pos[bb];
+      if (n0 < qr + kr) {
+        const int dd = (n0 < qr ? n0 : n0 - qr) % hd;
+        pr.cs[j] = *reinterpret_cast<const float4*>(rope + static_cast<size_t>(p) * (hd / 2) + dd / 2);
+      }
+      if (n0 >= qr) pr.blk[j] = bt[static_cast<size_t>(rows.slot[bb]) * mb + (p >> 4)];
+    }
+    return pr;
+  }
+
+  template <int JT>
+  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane, const Pre& pr) const {
     const int n0 = 16 * nt + 4 * (lane >> 4);
     const int qr = H * hd, kr = Hkv * hd;
 #pragma unroll
@@ -250,9 +284,7 @@ struct EpiQKV {
       float v0 = acc[j][0] * s, v1 = acc[j][1] * s, v2 = acc[j][2] * s, v3 = acc[j][3] * s;
       const int p = rows.pos[b];
       if (n0 < qr + kr) {
-        const int dd = (n0 < qr ? n0 : n0 - qr) % hd;
-        const float2* rp = rope + static_cast<size_t>(p) * (hd / 2) + dd / 2;
-        const float2 c0 = rp[0], c1 = rp[1];
+        const float2 c0 = make_float2(pr.cs[j].x, pr.cs[j].y), c1 = make_float2(pr.cs[j].z, pr.cs[j].w);
         const float a0 = v0 * c0.x - v1 * c0.y, a1 = v0 * c0.y + v1 * c0.x;
         const float a2 = v2 * c1.x - v3 * c1.y, a3 = v2 * c1.y + v3 * c1.x;
         v0 = a0;
@@ -264,7 +296,7 @@ struct EpiQKV {
         *reinterpret_cast<float4*>(q + static_cast<size_t>(b) * qr + n0) = make_float4(v0, v1, v2, v3);
         continue;
       }
-      const int blk = bt[static_cast<size_t>(rows.slot[b]) * mb + (p >> 4)];
+      const int blk = pr.blk[j];
       const int off = p & 15;
       if (n0 < qr + kr) {
         const int m = n0 - qr, kvh = m / hd, dd = m % hd;
@@ -294,15 +326,32 @@ struct EpiResid {
   float* x;                     // residual [rows][d]
   typename P::elem* act;        // next activation (K-block-major)
 
+  // The residual values this lane updates (row 0's for rows past n_rows).
+  // Each (row, feature) is read and written by one lane only.
+  struct Pre {
+    float4 x[kRows / 16];
+  };
   template <int JT>
-  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float*, int lane) const {
+  __device__ __forceinline__ Pre prefetch(int nt, int lane) const {
+    Pre pr;
+    const int n0 = 16 * nt + 4 * (lane >> 4);
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+      const int b = 16 * j + (lane & 15);
+      pr.x[j] = *reinterpret_cast<const float4*>(x + static_cast<size_t>(b < n_rows ? b : 0) * d + n0);
+    }
+    return pr;
+  }
+
+  template <int JT>
+  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float*, int lane, const Pre& pr) const {
     const int n0 = 16 * nt + 4 * (lane >> 4);
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
       const int b = 16 * j + (lane & 15);
       if (b >= n_rows) continue;
       float4* xp = reinterpret_cast<float4*>(x + static_cast<size_t>(b) * d + n0);
-      float4 xv = *xp;
+      float4 xv = pr.x[j];
       xv.x += acc[j][0];
       xv.y += acc[j][1];
       xv.z += acc[j][2];
@@ -322,8 +371,14 @@ struct EpiSwiGLU {
   float eps;
   typename P::elem* act;        // h, K-block-major over d_ff
 
+  struct Pre {};
   template <int JT>
-  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane) const {
+  __device__ __forceinline__ Pre prefetch(int, int) const {
+    return {};
+  }
+
+  template <int JT>
+  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane, const Pre&) const {
     const int j0 = 8 * nt + 2 * (lane >> 4);
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
@@ -350,8 +405,14 @@ struct EpiLogits {
   float2* part;                 // [tiles][kRows] (value, index bits)
   int out_row[kRows];           // logits row of each token row, -1 = none
 
+  struct Pre {};
   template <int JT>
-  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane) const {
+  __device__ __forceinline__ Pre prefetch(int, int) const {
+    return {};
+  }
+
+  template <int JT>
+  __device__ __forceinline__ void apply(int nt, const f32x4_t* acc, const float* ssq, int lane, const Pre&) const {
     const int n0 = 16 * nt + 4 * (lane >> 4);
 #pragma unroll
     for (int j = 0; j < JT; ++j) {

@@ -100,14 +100,18 @@ Layout layout(const Dims& d) {
   l.off_kc = take(l.kv_layer_stride * d.L);
   l.off_vc = take(l.kv_layer_stride * d.L);
   l.off_bt = take(static_cast<size_t>(d.S) * d.mb * sizeof(int32_t));
-  l.off_x = take(static_cast<size_t>(kMaxRows) * d.d * sizeof(float));
+  // Per-row buffers hold a whole prefill chunk (decode passes use the first rows).
+  l.off_x = take(static_cast<size_t>(kPrefillRows) * d.d * sizeof(float));
   // Activation records carry hi + lo parts for bf16 models.
-  l.act_bytes = static_cast<size_t>(d.kb_max) * kMaxRows * d.kblk * d.esize * (d.dtype == SPR_BF16 ? 2 : 1);
+  l.act_bytes = static_cast<size_t>(d.kb_max) * kPrefillRows * d.kblk * d.esize * (d.dtype == SPR_BF16 ? 2 : 1);
   l.off_act0 = take(l.act_bytes);
   l.off_act1 = take(l.act_bytes);
-  l.off_q = take(static_cast<size_t>(kMaxRows) * d.H * d.hd * sizeof(float));
+  l.off_q = take(static_cast<size_t>(kPrefillRows) * d.H * d.hd * sizeof(float));
   l.off_part = take(static_cast<size_t>(kMaxSplits) * d.H * (d.hd + 4) * sizeof(float));
   l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
+  l.off_prow = take(static_cast<size_t>(kPrefillRows) * 4 * sizeof(int32_t));
+  l.off_ptile = take(static_cast<size_t>(kPrefillTiles) * 4 * sizeof(int32_t));
+  l.off_rs = take(static_cast<size_t>(kPrefillRows) * sizeof(float));
   l.total = off;
   return l;
 }

@@ -1,9 +1,9 @@
 // C ABI of the decode library (include/sprout.h): argument validation, the
-// host-side slot table, and the launch sequence of one forward pass over a
-// set of token rows.
+// host-side slot table, and the launch sequences of a decode step and of a
+// prefill chunk.
 //
-// One forward pass (a decode step, or one prefill chunk of up to 128 token
-// rows) enqueues on the model's stream:
+// A decode step (one token row per active request) enqueues on the model's
+// stream:
 //   k_embed                      token rows -> fp32 residual x, activation
 //   per layer:
 //     k_stream_gemm<EpiQKV>      RMSNorm . Wqkv, RoPE, q out, k/v appended to the paged cache
@@ -13,6 +13,13 @@
 //     k_stream_gemm<EpiResid>    x += h W2^T
 //   k_stream_gemm<EpiLogits>     RMSNorm(x) Wlm^T, per-tile greedy candidates
 //   k_argmax_final               tok[slot] = lowest index of the row maximum
+// A prefill chunk (up to 1024 prompt rows of one or more requests) runs the
+// same layer stack on tiled, compute-bound kernels:
+//   k_embed_rows; per layer k_row_rscale, k_tile_gemm<EpiQKVRows>,
+//   k_attn_prefill (causal, 16 queries per MFMA), k_tile_gemm<EpiResidRows>,
+//   k_row_rscale, k_tile_gemm<EpiSwiGLURows>, k_tile_gemm<EpiResidRows>;
+//   then k_gather_rows of the rows that end a prompt, and the decode LM head.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -21,10 +28,14 @@
 #include "attn_kernels.h"
 #include "gemm_kernels.h"
 #include "host_state.h"
+#include "prefill_kernels.h"
 #include "step_kernels.h"
 #include "wgen_kernels.h"
 
 using namespace sprk;
+
+static_assert(spr::kPrefillRows == sprk::kPrefillRows, "prefill chunk size");
+static_assert(spr::kMaxRows == sprk::kRows, "decode pass size");
 
 struct spr_model {
   spr::Dims d{};
@@ -125,6 +136,9 @@ struct Ptrs {
   float* part() const { return reinterpret_cast<float*>(ws + l->off_part); }
   float2* amax() const { return reinterpret_cast<float2*>(ws + l->off_amax); }
   float2* rope() const { return reinterpret_cast<float2*>(ws + l->off_rope); }
+  PrefillRow* prow() const { return reinterpret_cast<PrefillRow*>(ws + l->off_prow); }
+  PrefillTile* ptile() const { return reinterpret_cast<PrefillTile*>(ws + l->off_ptile); }
+  float* rs() const { return reinterpret_cast<float*>(ws + l->off_rs); }
 };
 
 template <class P>
@@ -377,6 +391,127 @@ spr_status launch_projection(spr_model* m, int projection, int layer, int n) {
   }
 }
 
+// One prefill chunk: C rows (rows[] on the device), n_tiles attention query
+// tiles (ptile[] on the device), and the rows that end a prompt: emit_row[k]
+// (chunk row) emits request emit_out[k]'s first token into tok[emit_slot[k]].
+struct PrefillChunk {
+  int C = 0, n_tiles = 0, n_emit = 0;
+  int emit_row[kRows], emit_out[kRows], emit_slot[kRows];
+};
+
+template <class P, class KP, int HD>
+void launch_attn_prefill(spr_model* m, int layer, const PrefillChunk& ch, int Rp) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  const float qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
+  k_attn_prefill<KP, P, HD><<<dim3(ch.n_tiles, d.H), 256, 0, m->st>>>(p.q(), p.kc(layer), p.vc(layer), p.bt(),
+                                                                       p.ptile(), p.act(1), d.H, d.Hkv, d.mb, Rp,
+                                                                       qscale);
+}
+
+template <class P, class KP>
+spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  using E = typename P::elem;
+  const int C = ch.C;
+  const int Rp = 128 * ceil_div(C, 128);
+  const dim3 grid_d(ceil_div(d.d / 4, 64), C);
+  k_embed_rows<P><<<grid_d, 64, 0, m->st>>>(reinterpret_cast<const E*>(p.emb()), p.prow(), p.x(),
+                                            reinterpret_cast<E*>(p.act(0)), d.d, d.V, Rp);
+  SPR_LAUNCHED(m, "k_embed_rows");
+  auto tiles = [&](int NT) { return dim3(ceil_div(NT, 8), Rp / 128); };
+  for (int l = 0; l < d.L; ++l) {
+    k_row_rscale<<<ceil_div(C, 4), 256, 0, m->st>>>(p.x(), p.rs(), C, d.d, d.eps);
+    {
+      EpiQKVRows<P, KP> e{};
+      e.M = C;
+      e.H = d.H;
+      e.Hkv = d.Hkv;
+      e.hd = d.hd;
+      e.mb = d.mb;
+      e.q = p.q();
+      e.kc = reinterpret_cast<typename KP::elem*>(p.kc(l));
+      e.vc = reinterpret_cast<typename KP::elem*>(p.vc(l));
+      e.bt = p.bt();
+      e.rope = p.rope();
+      e.rows = p.prow();
+      e.rs = p.rs();
+      k_tile_gemm<P, EpiQKVRows<P, KP>><<<tiles(d.nt_qkv), 256, 0, m->st>>>(
+          reinterpret_cast<const uint4*>(p.wqkv(l)), reinterpret_cast<const uint4*>(p.act(0)), d.nt_qkv, d.kb_d, Rp,
+          e);
+    }
+    if (d.hd == 128) {
+      launch_attn_prefill<P, KP, 128>(m, l, ch, Rp);
+    } else {
+      launch_attn_prefill<P, KP, 64>(m, l, ch, Rp);
+    }
+    {
+      EpiResidRows<P> e{C, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      k_tile_gemm<P, EpiResidRows<P>><<<tiles(d.nt_o), 256, 0, m->st>>>(
+          reinterpret_cast<const uint4*>(p.wo(l)), reinterpret_cast<const uint4*>(p.act(1)), d.nt_o, d.kb_o, Rp, e);
+    }
+    k_row_rscale<<<ceil_div(C, 4), 256, 0, m->st>>>(p.x(), p.rs(), C, d.d, d.eps);
+    {
+      EpiSwiGLURows<P> e{C, Rp, p.rs(), reinterpret_cast<E*>(p.act(1))};
+      k_tile_gemm<P, EpiSwiGLURows<P>><<<tiles(d.nt_13), 256, 0, m->st>>>(
+          reinterpret_cast<const uint4*>(p.w13(l)), reinterpret_cast<const uint4*>(p.act(0)), d.nt_13, d.kb_d, Rp,
+          e);
+    }
+    {
+      EpiResidRows<P> e{C, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+      k_tile_gemm<P, EpiResidRows<P>><<<tiles(d.nt_2), 256, 0, m->st>>>(
+          reinterpret_cast<const uint4*>(p.w2(l)), reinterpret_cast<const uint4*>(p.act(1)), d.nt_2, d.kb_f, Rp, e);
+    }
+    SPR_LAUNCHED(m, "prefill layer");
+  }
+  if (ch.n_emit == 0) return SPR_OK;
+  const int n = ch.n_emit;
+  const int JT = n <= 16 ? 1 : n <= 32 ? 2 : n <= 64 ? 4 : 8;
+  {
+    GatherArgs g{};
+    g.x = p.x();
+    g.act = p.act(1);
+    g.d = d.d;
+    g.Rp = 16 * JT;
+    g.n = n;
+    for (int k = 0; k < n; ++k) g.src[k] = ch.emit_row[k];
+    k_gather_rows<P><<<dim3(ceil_div(d.d / 4, 64), n), 64, 0, m->st>>>(g);
+    SPR_LAUNCHED(m, "k_gather_rows");
+  }
+  spr_status st;
+  {
+    EpiLogits<P> e{};
+    e.n_rows = n;
+    e.V = d.V;
+    e.dnorm = d.d;
+    e.eps = d.eps;
+    e.logits = logits;
+    e.part = p.amax();
+    for (int k = 0; k < kRows; ++k) e.out_row[k] = k < n ? ch.emit_out[k] : -1;
+    if ((st = launch_gemm<P>(m, d.nt_lm, p.wlm(), p.act(1), d.kb_d, JT, e)) != SPR_OK) return st;
+  }
+  {
+    ArgmaxArgs a{};
+    a.part = p.amax();
+    a.tok_dev = tok;
+    a.n_tiles = d.nt_lm;
+    for (int k = 0; k < kRows; ++k) {
+      a.slot[k] = k < n ? ch.emit_slot[k] : 0;
+      a.out_row[k] = k < n ? ch.emit_out[k] : -1;
+    }
+    k_argmax_final<<<n, 256, 0, m->st>>>(a);
+    SPR_LAUNCHED(m, "k_argmax_final");
+  }
+  return SPR_OK;
+}
+
+spr_status prefill_any(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits) {
+  if (m->d.dtype == SPR_F32) return prefill_pass<F32, F32>(m, ch, tok, logits);
+  return m->d.kv_dtype == SPR_BF16 ? prefill_pass<BF16, BF16>(m, ch, tok, logits)
+                                   : prefill_pass<BF16, F32>(m, ch, tok, logits);
+}
+
 spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
                        bool do_lm) {
   if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, do_lm);
@@ -443,7 +578,7 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
   if (e == hipSuccess) e = hipMemsetAsync(p.bt(), 0, static_cast<size_t>(d.S) * d.mb * sizeof(int32_t), m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(0), 0, lay.act_bytes, m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(1), 0, lay.act_bytes, m->st);
-  if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kMaxRows) * d.d * sizeof(float), m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kPrefillRows) * d.d * sizeof(float), m->st);
   if (e == hipSuccess) e = hipStreamSynchronize(m->st);
   if (e != hipSuccess) {
     hip_fail(nullptr, "init", e);
@@ -478,37 +613,54 @@ spr_status spr_prefill(spr_model* m, int32_t n, const int32_t* slots, const int3
                               hipMemcpyHostToDevice, m->st));
   SPR_HIP(m, hipStreamSynchronize(m->st));
 
-  RowSet rs;
-  rs.n = 0;
-  auto flush = [&](bool any_emit) -> spr_status {
-    if (rs.n == 0) return SPR_OK;
-    for (int r = rs.n; r < kRows; ++r) {
-      rs.slot[r] = 0;
-      rs.pos[r] = 0;
-      rs.out_row[r] = -1;
-      rs.tok[r] = 0;
-    }
-    spr_status s2 = forward_any(m, rs, nullptr, tok, logits, any_emit);
-    rs.n = 0;
+  // Chunks of up to kPrefillRows rows in request order; a prompt may span
+  // chunks (its later rows attend to the positions an earlier chunk cached).
+  // The host tables of every chunk stay alive until the final synchronize.
+  std::vector<std::vector<PrefillRow>> row_tabs;
+  std::vector<std::vector<PrefillTile>> tile_tabs;
+  PrefillChunk ch;
+  std::vector<PrefillRow> chunk_rows;
+  std::vector<PrefillTile> tiles;
+  auto flush = [&]() -> spr_status {
+    if (chunk_rows.empty()) return SPR_OK;
+    ch.C = static_cast<int>(chunk_rows.size());
+    ch.n_tiles = static_cast<int>(tiles.size());
+    if (ch.n_tiles > spr::kPrefillTiles) return fail(SPR_ERR_INVALID_ARG, "internal: prefill tile table overflow");
+    row_tabs.push_back(std::move(chunk_rows));
+    tile_tabs.push_back(std::move(tiles));
+    chunk_rows = {};
+    tiles = {};
+    SPR_HIP(m, hipMemcpyAsync(p.prow(), row_tabs.back().data(), row_tabs.back().size() * sizeof(PrefillRow),
+                              hipMemcpyHostToDevice, m->st));
+    SPR_HIP(m, hipMemcpyAsync(p.ptile(), tile_tabs.back().data(), tile_tabs.back().size() * sizeof(PrefillTile),
+                              hipMemcpyHostToDevice, m->st));
+    spr_status s2 = prefill_any(m, ch, tok, logits);
+    ch = PrefillChunk{};
     return s2;
   };
   int64_t t = 0;
-  bool any_emit = false;
   for (int i = 0; i < n; ++i) {
-    for (int pos = 0; pos < seq_lens[i]; ++pos, ++t) {
-      const int r = rs.n++;
-      rs.slot[r] = slots[i];
-      rs.pos[r] = pos;
-      rs.tok[r] = tokens[t];
-      rs.out_row[r] = pos == seq_lens[i] - 1 ? i : -1;
-      any_emit |= rs.out_row[r] >= 0;
-      if (rs.n == kRows) {
-        if ((st = flush(any_emit)) != SPR_OK) return st;
-        any_emit = false;
+    int pos = 0;
+    while (pos < seq_lens[i]) {
+      if (static_cast<int>(chunk_rows.size()) == spr::kPrefillRows) {
+        if ((st = flush()) != SPR_OK) return st;
+      }
+      // The next segment of request i that fits this chunk, in query tiles of 16.
+      const int seg = std::min(seq_lens[i] - pos, spr::kPrefillRows - static_cast<int>(chunk_rows.size()));
+      const int row0 = static_cast<int>(chunk_rows.size());
+      for (int k = 0; k < seg; ++k, ++t) chunk_rows.push_back(PrefillRow{slots[i], pos + k, tokens[t], 0});
+      for (int k = 0; k < seg; k += 16) tiles.push_back(PrefillTile{slots[i], row0 + k, std::min(16, seg - k), pos + k});
+      pos += seg;
+      if (pos == seq_lens[i]) {
+        ch.emit_row[ch.n_emit] = row0 + seg - 1;
+        ch.emit_out[ch.n_emit] = i;
+        ch.emit_slot[ch.n_emit] = slots[i];
+        ++ch.n_emit;
       }
     }
   }
-  if ((st = flush(any_emit)) != SPR_OK) return st;
+  if ((st = flush()) != SPR_OK) return st;
+  SPR_HIP(m, hipStreamSynchronize(m->st));
   return SPR_OK;
 }
 

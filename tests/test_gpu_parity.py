@@ -112,6 +112,10 @@ TOY_CASES = {
     "bf16_long_context_splits": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=128, vocab=500),
         [700, 300], [20, 3]),
+    # Prompts spanning prefill chunks (1024 rows): 1500 crosses the first boundary, 700 the second.
+    "bf16_prompts_across_chunks": (
+        ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
+        [1500, 7, 700, 40], [3, 4, 2, 5]),
 }
 
 
