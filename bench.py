@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode tokens/s + achieved HBM GB/s, Llama-2-7B-shape bf16, ragged batch 32"
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
 DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16>, 2, 8, true>"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_gemm_pmc_llama2_7b_b8.txt")
 
@@ -143,6 +144,35 @@ hbm_bytes_per_launch = {fetch_b + write_b:.0f}
 kernel_source_hash = {kernel_source_hash()}
 """)
     print(open(TRAFFIC_PROFILE).read())
+
+
+def time_prefill(model, m, wl, stops, reps: int = 3):
+    """Prefill of the whole batch (every prompt, chunks of up to 1024 rows),
+    re-run on freed slots.  Algorithmic flops: 2 x weight elements of the layer
+    stack per prompt token, 4 x hd x H x (positions attended) per token and layer
+    for attention, and the LM head for each prompt's last row; bf16 models issue
+    twice the projection MFMA work (hi + lo activation parts)."""
+    import torch
+    B = wl.batch
+    tokens = int(sum(len(t) for t in wl.tokens))
+    layer_w = m.weight_elements_per_step() - m.vocab * m.d_model     # projections of all layers
+    att = sum(n * (n + 1) // 2 for n in (len(t) for t in wl.tokens)) * 4 * m.head_dim * m.n_heads * m.n_layers
+    flops = 2.0 * layer_w * tokens + att + 2.0 * m.vocab * m.d_model * B
+    tok = model.new_token_buffer()
+    times = []
+    for _ in range(reps + 1):
+        for i in range(B):
+            model.free_slot(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        model.prefill(list(range(B)), wl.tokens, stops, tok)   # synchronous
+        times.append(time.perf_counter() - t0)
+    ms = 1e3 * min(times[1:])
+    tflops = flops / (ms * 1e-3) / 1e12
+    issue = 2.0 if m.bf16 else 1.0
+    return {"tokens": tokens, "ms": round(ms, 2), "tokens_per_s": round(tokens / (ms * 1e-3), 1),
+            "algorithmic_tflops": round(tflops, 1), "mfma_issued_tflops": round(tflops * issue, 1),
+            "peak_tflops": PEAK_BF16_TFLOPS, "mfma_frac": round(tflops * issue / PEAK_BF16_TFLOPS, 4)}
 
 
 def cpu_baseline(cfg, wl, seconds: float):
@@ -301,6 +331,8 @@ def main():
                      "traffic": traffic, "bytes_per_launch": per_launch, "us_per_launch": round(us, 3),
                      "other_projections": others},
     }
+    out["prefill"] = time_prefill(model, m, wl, stops)
+    log(f"prefill: {out['prefill']}")
     model.close()
     del model
     torch.cuda.empty_cache()

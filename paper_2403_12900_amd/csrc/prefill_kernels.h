@@ -56,88 +56,153 @@ __global__ __launch_bounds__(256) void k_row_rscale(const float* __restrict__ x,
   if (lane == 0) rs[b] = rsqrtf(s / static_cast<float>(d) + eps);
 }
 
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Waits until at most N vector-memory operations of this wave are in flight
+// (expcnt and lgkmcnt not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// 16-byte LDS read issued as plain ds_read_b128.  The compiler treats LDS
+// that global_load_lds fills as possibly still in flight and, at loop
+// back-edges, would wait for every load in flight (vmcnt(0)) before any LDS
+// read; the kernel's own vmcnt wait plus barrier already orders the read, so
+// the read bypasses that tracking.  The caller waits with lds_reads_done()
+// before using the results.
+__device__ __forceinline__ u32x4_t lds_read16(const uint4* p) {
+  u32x4_t v;
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<size_t>((lds_void*)p));
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+__device__ __forceinline__ void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Ties a value read by lds_read16 to a point after lds_reads_done(): volatile
+// asm statements keep their order, so no use of v can move above the wait.
+__device__ __forceinline__ void lds_value_ready(u32x4_t& v) { asm volatile("" : "+v"(v)); }
+
+// Work-group barrier for LDS filled by global_load_lds: each wave first waits
+// for its own loads (vmcnt), so after the barrier every wave's fragments of
+// that stage are in LDS.  No memory fence: a workgroup fence here would wait
+// for every load in flight (vmcnt(0)), including the stages being prefetched.
+// The empty asm statements keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void lds_stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Tiled projection: out[b][n] = sum_k W[n][k] x[b][k] for rows b < M, fused
-// with the op that follows (Epi).  Work-group = 128 output features (8 weight
-// tiles) x 128 rows; per K-block its 256 threads copy the 8 weight fragments
-// and the 8 x parts activation fragments (1 KiB each) into LDS, and each wave
-// multiplies a 64 x 64 quarter: 4 weight x 4 activation operands, all parts,
-// 16 x parts MFMAs.  Two LDS stages: the next K-block's global loads are in
-// flight while the current one is multiplied.  Activation fragments are
-// stored to LDS in MFMA lane order (lane r + 16 g <- row r, K-group g), so
-// every operand read is one conflict-free 16-byte LDS load.
-template <class P, class Epi>
+// with the op that follows (Epi).  A work-group computes TN weight tiles (16
+// output features each) x TM row tiles (16 rows each) with four waves, each
+// owning a WN x WM block of 16 x 16 MFMA tiles.  Per K-block the work-group's
+// operands -- TN weight fragments and TM x parts activation fragments, 1 KiB
+// each -- go from global memory straight into LDS (global_load_lds, no
+// register staging) in MFMA lane order: weight fragments are stored that way,
+// and for activation fragments lane r + 16 g fetches row r's K-group g.  Three
+// LDS stages (three separate arrays, so the compiler tracks each stage's
+// loads on its own) keep two K-blocks in flight; each K-block costs one
+// barrier: wait for its own loads, barrier (which also frees the stage read
+// one K-block earlier), issue the loads two K-blocks ahead, multiply.  Weight
+// tiles past NT re-read tile NT - 1 and are not stored.
+template <int TN, int TM>
+struct TileShape {
+  static constexpr int GN = TN == 4 && TM == 8 ? 1 : 2;  // waves along features
+  static constexpr int GM = 4 / GN;                     // waves along rows
+  static constexpr int WN = TN / GN, WM = TM / GM;
+  static_assert(GN * GM == 4 && WN * GN == TN && WM * GM == TM, "tile shape");
+};
+
+template <class P, int TN, int TM, class Epi>
 __global__ __launch_bounds__(256) void k_tile_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X, int NT,
                                                    int KB, int Rp, Epi epi) {
   constexpr int PARTS = P::parts;
-  constexpr int NFRAG = 8 + 8 * PARTS;  // fragments per K-block stage
-  constexpr int PER = NFRAG / 4;        // fragments each thread copies
-  __shared__ uint4 lds[2][NFRAG][64];
+  constexpr int NFRAG = TN + TM * PARTS;
+  static_assert(NFRAG % 4 == 0, "fragments per stage must split over four waves");
+  constexpr int L = NFRAG / 4;  // loads per wave per stage
+  using TS = TileShape<TN, TM>;
+  constexpr int WN = TS::WN, WM = TS::WM;
+  __shared__ uint4 st0[NFRAG][64];
+  __shared__ uint4 st1[NFRAG][64];
+  __shared__ uint4 st2[NFRAG][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nt0 = blockIdx.x * 8, m0 = blockIdx.y * 128;
-  const int fw = wave & 1, tw = wave >> 1;
+  const int nt0 = blockIdx.x * TN, m0 = blockIdx.y * TM * 16;
+  const int wn = wave % TS::GN, wm = wave / TS::GN;
   const size_t xpart = static_cast<size_t>(Rp) * 4;  // uint4 per (K-block, part)
-  // Thread's copy duty: fragment wave + 4 i, lane `lane`.  Activation
-  // fragments go to the LDS slot of MFMA lane (lane >> 2) + 16 (lane & 3).
-  const int xslot = (lane >> 2) + 16 * (lane & 3);
+  const int xlane = (lane & 15) * 4 + (lane >> 4);   // uint4 of an activation fragment MFMA lane `lane` needs
 
-  auto load = [&](uint4* r, int kb) {
+  auto issue = [&](int kb, uint4(*dst)[64]) {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
+    for (int i = 0; i < L; ++i) {
       const int f = wave + 4 * i;
-      if (f < 8) {
-        const int nt = nt0 + f;
-        r[i] = nt < NT ? load_weight<true>(W + (static_cast<size_t>(nt) * KB + kb) * 64 + lane)
-                       : make_uint4(0u, 0u, 0u, 0u);
+      const uint4* src;
+      if (f < TN) {
+        const int nt = min(nt0 + f, NT - 1);
+        src = W + (static_cast<size_t>(nt) * KB + kb) * 64 + lane;
       } else {
-        const int a = f - 8, q = a >> 3, tt = a & 7;
-        r[i] = X[(static_cast<size_t>(kb) * PARTS + q) * xpart + static_cast<size_t>(m0 + 16 * tt) * 4 + lane];
+        const int a = f - TN, q = a / TM, tt = a % TM;
+        src = X + (static_cast<size_t>(kb) * PARTS + q) * xpart + static_cast<size_t>(m0 + 16 * tt) * 4 + xlane;
       }
-    }
-  };
-  auto store = [&](int s, const uint4* r) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int f = wave + 4 * i;
-      lds[s][f][f < 8 ? lane : xslot] = r[i];
+      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)&dst[f][0], 16, 0, 0);
     }
   };
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[WN][WM];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < WN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < WM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  uint4 pre[PER];
-  load(pre, 0);
-  store(0, pre);
-  __syncthreads();
-  for (int kb = 0; kb < KB; ++kb) {
-    const int s = kb & 1;
-    if (kb + 1 < KB) load(pre, kb + 1);
-    uint4 a[4], b[4][PARTS];
+  // K-block kb: its loads are the oldest in flight; the next K-block's (if
+  // any) may stay in flight.  Then the stage read at kb - 1 is free for kb + 2.
+  auto step = [&](int kb, uint4(*cur)[64], uint4(*next)[64]) {
+    if (kb + 1 < KB) {
+      wait_vmem<L>();
+    } else {
+      wait_vmem<0>();
+    }
+    lds_stage_barrier();
+    if (kb + 2 < KB) issue(kb + 2, next);
+    u32x4_t a[WN], b[WM][PARTS];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = lds[s][fw * 4 + i][lane];
+    for (int i = 0; i < WN; ++i) a[i] = lds_read16(&cur[wn * WN + i][lane]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < WM; ++j)
 #pragma unroll
-      for (int q = 0; q < PARTS; ++q) b[j][q] = lds[s][8 + 8 * q + tw * 4 + j][lane];
+      for (int q = 0; q < PARTS; ++q) b[j][q] = lds_read16(&cur[TN + q * TM + wm * WM + j][lane]);
+    lds_reads_done();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < WN; ++i) lds_value_ready(a[i]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < WM; ++j)
 #pragma unroll
-        for (int q = 0; q < PARTS; ++q) acc[i][j] = P::mma(acc[i][j], a[i], b[j][q]);
-    if (kb + 1 < KB) store(s ^ 1, pre);
-    __syncthreads();
+      for (int q = 0; q < PARTS; ++q) lds_value_ready(b[j][q]);
+#pragma unroll
+    for (int i = 0; i < WN; ++i)
+#pragma unroll
+      for (int j = 0; j < WM; ++j)
+#pragma unroll
+        for (int q = 0; q < PARTS; ++q)
+          acc[i][j] = P::mma(acc[i][j], __builtin_bit_cast(uint4, a[i]), __builtin_bit_cast(uint4, b[j][q]));
+  };
+
+  issue(0, st0);
+  if (KB > 1) issue(1, st1);
+  for (int kb = 0; kb < KB; kb += 3) {
+    step(kb, st0, st2);
+    if (kb + 1 < KB) step(kb + 1, st1, st0);
+    if (kb + 2 < KB) step(kb + 2, st2, st1);
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int nt = nt0 + fw * 4 + i;
+  for (int i = 0; i < WN; ++i) {
+    const int nt = nt0 + wn * WN + i;
     if (nt >= NT) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) epi.apply_tile(nt, m0 + tw * 64 + 16 * j, acc[i][j], lane);
+    for (int j = 0; j < WM; ++j) epi.apply_tile(nt, m0 + 16 * (wm * WM + j), acc[i][j], lane);
   }
 }
 

@@ -409,6 +409,22 @@ void launch_attn_prefill(spr_model* m, int layer, const PrefillChunk& ch, int Rp
                                                                        qscale);
 }
 
+// Tile shape of a prefill projection: 128 x 128 work-groups when that gives
+// at least 512 of them, else 64 features x 128 rows, else 64 x 64.
+template <class P, class Epi>
+void launch_tile_gemm(hipStream_t st, const char* W, const char* X, int NT, int KB, int Rp, const Epi& e) {
+  const uint4* w = reinterpret_cast<const uint4*>(W);
+  const uint4* x = reinterpret_cast<const uint4*>(X);
+  const int mt = Rp / 128;
+  if (ceil_div(NT, 8) * mt >= 512) {
+    k_tile_gemm<P, 8, 8, Epi><<<dim3(ceil_div(NT, 8), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+  } else if (ceil_div(NT, 4) * mt >= 512) {
+    k_tile_gemm<P, 4, 8, Epi><<<dim3(ceil_div(NT, 4), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+  } else {
+    k_tile_gemm<P, 4, 4, Epi><<<dim3(ceil_div(NT, 4), Rp / 64), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+  }
+}
+
 template <class P, class KP>
 spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits) {
   const spr::Dims& d = m->d;
@@ -420,7 +436,6 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
   k_embed_rows<P><<<grid_d, 64, 0, m->st>>>(reinterpret_cast<const E*>(p.emb()), p.prow(), p.x(),
                                             reinterpret_cast<E*>(p.act(0)), d.d, d.V, Rp);
   SPR_LAUNCHED(m, "k_embed_rows");
-  auto tiles = [&](int NT) { return dim3(ceil_div(NT, 8), Rp / 128); };
   for (int l = 0; l < d.L; ++l) {
     k_row_rscale<<<ceil_div(C, 4), 256, 0, m->st>>>(p.x(), p.rs(), C, d.d, d.eps);
     {
@@ -437,9 +452,7 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
       e.rope = p.rope();
       e.rows = p.prow();
       e.rs = p.rs();
-      k_tile_gemm<P, EpiQKVRows<P, KP>><<<tiles(d.nt_qkv), 256, 0, m->st>>>(
-          reinterpret_cast<const uint4*>(p.wqkv(l)), reinterpret_cast<const uint4*>(p.act(0)), d.nt_qkv, d.kb_d, Rp,
-          e);
+      launch_tile_gemm<P>(m->st, p.wqkv(l), p.act(0), d.nt_qkv, d.kb_d, Rp, e);
     }
     if (d.hd == 128) {
       launch_attn_prefill<P, KP, 128>(m, l, ch, Rp);
@@ -448,20 +461,16 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
     }
     {
       EpiResidRows<P> e{C, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      k_tile_gemm<P, EpiResidRows<P>><<<tiles(d.nt_o), 256, 0, m->st>>>(
-          reinterpret_cast<const uint4*>(p.wo(l)), reinterpret_cast<const uint4*>(p.act(1)), d.nt_o, d.kb_o, Rp, e);
+      launch_tile_gemm<P>(m->st, p.wo(l), p.act(1), d.nt_o, d.kb_o, Rp, e);
     }
     k_row_rscale<<<ceil_div(C, 4), 256, 0, m->st>>>(p.x(), p.rs(), C, d.d, d.eps);
     {
       EpiSwiGLURows<P> e{C, Rp, p.rs(), reinterpret_cast<E*>(p.act(1))};
-      k_tile_gemm<P, EpiSwiGLURows<P>><<<tiles(d.nt_13), 256, 0, m->st>>>(
-          reinterpret_cast<const uint4*>(p.w13(l)), reinterpret_cast<const uint4*>(p.act(0)), d.nt_13, d.kb_d, Rp,
-          e);
+      launch_tile_gemm<P>(m->st, p.w13(l), p.act(0), d.nt_13, d.kb_d, Rp, e);
     }
     {
       EpiResidRows<P> e{C, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      k_tile_gemm<P, EpiResidRows<P>><<<tiles(d.nt_2), 256, 0, m->st>>>(
-          reinterpret_cast<const uint4*>(p.w2(l)), reinterpret_cast<const uint4*>(p.act(1)), d.nt_2, d.kb_f, Rp, e);
+      launch_tile_gemm<P>(m->st, p.w2(l), p.act(1), d.nt_2, d.kb_f, Rp, e);
     }
     SPR_LAUNCHED(m, "prefill layer");
   }
