@@ -178,6 +178,51 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
  */
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
 
+/* One request of a serving run (host memory, read during the call). */
+typedef struct {
+  const int32_t* tokens; /* prompt: directive prefix followed by the user prompt */
+  int32_t n_tokens;      /* >= 1 */
+  int32_t stop_len;      /* tokens to generate, >= 1; n_tokens + stop_len - 1 <= max_ctx */
+  int32_t arrival;       /* first scheduler iteration it may be admitted in (0 = at once) */
+} spr_request;
+
+typedef struct {
+  int64_t iterations;    /* scheduler iterations run */
+  int64_t decode_steps;  /* decode steps launched */
+  int64_t prefill_calls; /* batched prefills launched */
+  int64_t decode_tokens; /* tokens produced by decode steps */
+  int32_t max_batch;     /* largest decode batch */
+  double mean_batch;     /* mean decode batch */
+} spr_serve_stats;
+
+/*
+ * Serves n requests with continuous (iteration-level) batching: the
+ * scheduling of the inference servers the paper deploys on (Section IV:
+ * vLLM's paged KV cache; related work: Orca's iteration-level batching),
+ * here over the decode step above.  Every iteration
+ *   1. admits waiting requests, first come first served, whose arrival
+ *      iteration has come, into free slots while fewer than max_active
+ *      requests are in flight and the KV pool can reserve their blocks (a
+ *      request that does not fit yet holds back the ones behind it);
+ *   2. prefills the admitted requests together (first tokens);
+ *   3. runs one decode step over every request still generating;
+ *   4. retires requests that reached their stop length, freeing their slots
+ *      and KV blocks for the next iteration.
+ * Iterations with nothing in flight skip to the next arrival.  Outputs are
+ * the same greedy tokens each request would get served alone.
+ *   max_active 1..max_slots
+ *   tok        device int32 [max_slots]: scratch token buffer, indexed by slot
+ *   out        device int32 [sum of stop_len]: request i's tokens at offset
+ *              stop_len[0] + ... + stop_len[i-1]
+ *   stats      host, or NULL
+ * Needs every slot free on entry (SPR_ERR_STATE otherwise) and leaves them
+ * free.  A malformed request, or one that max_ctx or the KV pool could never
+ * hold, fails with SPR_ERR_INVALID_ARG before any work is enqueued.
+ * Synchronous: out is complete when it returns.
+ */
+spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t* tok,
+                     int32_t* out, spr_serve_stats* stats);
+
 /* Releases the host state.  The workspace is the caller's to free afterwards. */
 spr_status spr_release(spr_model* m);
 

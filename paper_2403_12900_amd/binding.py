@@ -41,6 +41,16 @@ _I32P = ctypes.POINTER(ctypes.c_int32)
 _lib = None
 
 
+class SprRequest(ctypes.Structure):
+    _fields_ = [("tokens", _I32P), ("n_tokens", ctypes.c_int32), ("stop_len", ctypes.c_int32),
+                ("arrival", ctypes.c_int32)]
+
+
+class SprServeStats(ctypes.Structure):
+    _fields_ = [("iterations", ctypes.c_int64), ("decode_steps", ctypes.c_int64), ("prefill_calls", ctypes.c_int64),
+                ("decode_tokens", ctypes.c_int64), ("max_batch", ctypes.c_int32), ("mean_batch", ctypes.c_double)]
+
+
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     global _lib
     if _lib is not None:
@@ -71,6 +81,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_time_projection.restype = ctypes.c_int
     L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_float)]
+    L.spr_serve.restype = ctypes.c_int
+    L.spr_serve.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(SprRequest), ctypes.c_int32, vp, vp,
+                            ctypes.POINTER(SprServeStats)]
     L.spr_release.restype = ctypes.c_int
     L.spr_release.argtypes = [vp]
     L.spr_last_error.restype = ctypes.c_char_p
@@ -182,6 +195,27 @@ class DecodeModel:
         out = ctypes.c_float()
         _check(self.lib.spr_time_projection(self.h, self.PROJECTIONS[projection], n_rows, reps, ctypes.byref(out)))
         return float(out.value)
+
+    def serve(self, prompts: Sequence[Sequence[int]], stop_lens: Sequence[int], max_active: int,
+              arrivals: Optional[Sequence[int]] = None):
+        """Continuous batching of all requests (spr_serve); returns (tokens per request, stats dict)."""
+        n = len(prompts)
+        arrivals = [0] * n if arrivals is None else list(arrivals)
+        keep = [_i32(p) for p in prompts]
+        reqs = (SprRequest * max(n, 1))()
+        for i in range(n):
+            reqs[i] = SprRequest(_ptr(keep[i]), len(keep[i]), int(stop_lens[i]), int(arrivals[i]))
+        total = int(sum(stop_lens))
+        out = self.torch.full((max(total, 1),), -1, dtype=self.torch.int32, device=self.device)
+        tok = self.new_token_buffer()
+        st = SprServeStats()
+        _check(self.lib.spr_serve(self.h, n, reqs, max_active, ctypes.c_void_p(tok.data_ptr()),
+                                  ctypes.c_void_p(out.data_ptr()), ctypes.byref(st)))
+        flat = out.cpu().numpy()
+        off = np.concatenate([[0], np.cumsum(np.asarray(stop_lens, dtype=np.int64))]).astype(int)
+        toks = [flat[off[i]:off[i + 1]].copy() for i in range(n)]
+        stats = {f: getattr(st, f) for f, _ in SprServeStats._fields_}
+        return toks, stats
 
     def close(self):
         if getattr(self, "h", None) is not None and self.h.value:

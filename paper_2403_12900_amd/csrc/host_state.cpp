@@ -275,4 +275,132 @@ void SlotTable::block_row(int slot, int32_t* row) const {
   for (int b = 0; b < d_.mb; ++b) row[b] = b < static_cast<int>(sl.blocks.size()) ? sl.blocks[b] : 0;
 }
 
+spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs, int max_active, ServeDevice& dev,
+                 ServeCounters* counters, std::string* err) {
+  if (n < 0 || (n > 0 && reqs == nullptr)) {
+    *err = "serve: n must be >= 0 and requests non-null";
+    return SPR_ERR_INVALID_ARG;
+  }
+  if (max_active < 1 || max_active > d.S) {
+    *err = "serve: max_active must be in [1, max_slots]";
+    return SPR_ERR_INVALID_ARG;
+  }
+  for (int s = 0; s < d.S; ++s) {
+    if (tab.slot(s).state != kFree) {
+      *err = "serve: every slot must be free";
+      return SPR_ERR_STATE;
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    const ServeRequest& r = reqs[i];
+    if (r.tokens == nullptr || r.n_tokens < 1 || r.stop_len < 1 || r.arrival < 0) {
+      *err = "serve: request " + std::to_string(i) + " is malformed";
+      return SPR_ERR_INVALID_ARG;
+    }
+    for (int t = 0; t < r.n_tokens; ++t) {
+      if (r.tokens[t] < 0 || r.tokens[t] >= d.V) {
+        *err = "serve: request " + std::to_string(i) + " has a token id out of range";
+        return SPR_ERR_INVALID_ARG;
+      }
+    }
+    if (static_cast<int64_t>(r.n_tokens) + r.stop_len - 1 > d.max_ctx ||
+        SlotTable::blocks_for(r.n_tokens, r.stop_len) > tab.free_blocks()) {
+      *err = "serve: request " + std::to_string(i) + " can never fit (max_ctx or KV pool)";
+      return SPR_ERR_INVALID_ARG;
+    }
+  }
+  struct Live {
+    int slot, req, len, produced;
+  };
+  std::vector<Live> live;
+  std::vector<char> busy(d.S, 0);
+  ServeCounters c;
+  int64_t batch_sum = 0;
+  int q = 0;
+  int it = 0;
+  std::vector<int32_t> s0, s1, s2, s3, s4, ret;
+  while (q < n || !live.empty()) {
+    dev.iteration = it;
+    // 1-2: admissions and their prefill.
+    s0.clear();
+    s1.clear();
+    s2.clear();
+    s3.clear();
+    int reserve = 0;
+    while (q < n && reqs[q].arrival <= it && static_cast<int>(live.size() + s0.size()) < max_active) {
+      const int need = SlotTable::blocks_for(reqs[q].n_tokens, reqs[q].stop_len);
+      if (need > tab.free_blocks() - reserve) break;
+      int slot = 0;
+      while (busy[slot]) ++slot;
+      busy[slot] = 1;
+      reserve += need;
+      s0.push_back(slot);
+      s1.push_back(q);
+      s2.push_back(reqs[q].n_tokens);
+      s3.push_back(reqs[q].stop_len);
+      ++q;
+    }
+    if (!s0.empty()) {
+      const int k = static_cast<int>(s0.size());
+      spr_status st = tab.check_prefill(k, s0.data(), s2.data(), s3.data(), err);
+      if (st != SPR_OK) return st;
+      ret.assign(k, 0);
+      tab.commit_prefill(k, s0.data(), s2.data(), s3.data(), ret.data());
+      if ((st = dev.prefill(k, s0.data(), s1.data())) != SPR_OK) return st;
+      ++c.prefill_calls;
+      for (int i = 0; i < k; ++i) {
+        if (ret[i]) {
+          tab.commit_free(s0[i]);
+          busy[s0[i]] = 0;
+        } else {
+          live.push_back(Live{s0[i], s1[i], s2[i], 1});
+        }
+      }
+    }
+    // 3-4: one decode step, retirements.
+    if (!live.empty()) {
+      const int k = static_cast<int>(live.size());
+      s0.resize(k);
+      s1.resize(k);
+      s2.resize(k);
+      s4.resize(k);
+      for (int i = 0; i < k; ++i) {
+        s0[i] = live[i].slot;
+        s1[i] = live[i].len;
+        s2[i] = live[i].req;
+        s4[i] = live[i].produced;
+      }
+      spr_status st = tab.check_decode(k, s0.data(), s1.data(), err);
+      if (st != SPR_OK) return st;
+      if ((st = dev.decode(k, s0.data(), s1.data(), s2.data(), s4.data())) != SPR_OK) return st;
+      ret.assign(k, 0);
+      tab.commit_decode(k, s0.data(), ret.data());
+      ++c.decode_steps;
+      c.decode_tokens += k;
+      batch_sum += k;
+      if (k > c.max_batch) c.max_batch = k;
+      std::vector<Live> keep;
+      keep.reserve(k);
+      for (int i = 0; i < k; ++i) {
+        Live l = live[i];
+        l.len += 1;
+        l.produced += 1;
+        if (ret[i]) {
+          tab.commit_free(l.slot);
+          busy[l.slot] = 0;
+        } else {
+          keep.push_back(l);
+        }
+      }
+      live.swap(keep);
+    }
+    ++c.iterations;
+    ++it;
+    if (live.empty() && q < n && reqs[q].arrival > it) it = reqs[q].arrival;  // idle until the next arrival
+  }
+  c.mean_batch = c.decode_steps > 0 ? static_cast<double>(batch_sum) / c.decode_steps : 0.0;
+  if (counters) *counters = c;
+  return SPR_OK;
+}
+
 }  // namespace spr

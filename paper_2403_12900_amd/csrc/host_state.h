@@ -75,10 +75,59 @@ class SlotTable {
   // Block-table row of a slot, padded with 0 to `mb` entries.
   void block_row(int slot, int32_t* row) const;
 
+  // KV blocks a request of this prompt and stop length reserves.
+  static int blocks_for(int seq_len, int stop_len) { return (seq_len + stop_len - 1 + kKvBlock - 1) / kKvBlock; }
+
  private:
   Dims d_{};
   std::vector<Slot> slots_;
   std::vector<int32_t> free_;   // stack of free block ids
 };
+
+// ---------------------------------------------------------------------------
+// Continuous (iteration-level) batching over the slot table.  Requests wait
+// in arrival order; every scheduler iteration
+//   1. admits waiting requests whose arrival iteration has come, first come
+//      first served, into free slots while fewer than max_active requests are
+//      in flight and the KV pool can reserve their blocks (a request that
+//      does not fit yet holds back the ones behind it);
+//   2. prefills the admitted requests together (each emits its first token);
+//   3. runs one decode step over every request still generating;
+//   4. retires requests that produced their stop length and frees their slots
+//      and blocks at once, for the next iteration's admissions.
+// Iterations with nothing in flight jump to the next arrival.  The device
+// work goes through ServeDevice, so the policy runs unchanged on the host
+// alone (tests) or over the GPU kernels (spr_serve).
+// ---------------------------------------------------------------------------
+struct ServeRequest {
+  const int32_t* tokens;  // prompt (directive prefix ++ user prompt)
+  int n_tokens, stop_len;
+  int arrival;            // first scheduler iteration it may be admitted in
+};
+
+struct ServeCounters {
+  int64_t iterations = 0, decode_steps = 0, prefill_calls = 0, decode_tokens = 0;
+  int max_batch = 0;
+  double mean_batch = 0.0;  // mean decode-step batch
+};
+
+class ServeDevice {
+ public:
+  int iteration = 0;  // scheduler iteration of the next call (set by serve)
+  virtual ~ServeDevice() = default;
+  // Prefill requests req[k] into slots[k] (already reserved in the table);
+  // each emits its token 0.
+  virtual spr_status prefill(int n, const int32_t* slots, const int32_t* req) = 0;
+  // One decode step; row k: slot, cached positions, request, index of the
+  // token the step produces for it.
+  virtual spr_status decode(int n, const int32_t* slots, const int32_t* lens, const int32_t* req,
+                            const int32_t* produced) = 0;
+};
+
+// Runs the whole request list.  Needs every slot free on entry; leaves every
+// slot free on success.  SPR_ERR_INVALID_ARG for a malformed request or one
+// the KV pool could never hold; errors of the device calls are returned as is.
+spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs, int max_active, ServeDevice& dev,
+                 ServeCounters* counters, std::string* err);
 
 }  // namespace spr

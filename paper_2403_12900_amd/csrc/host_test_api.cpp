@@ -3,6 +3,7 @@
 // spr_prefill / spr_decode_step call runs before enqueueing work can be
 // exercised without a GPU.  Not part of the device library.
 #include <string>
+#include <vector>
 
 #include "host_state.h"
 
@@ -83,4 +84,62 @@ int sprh_slot(void* hp, int slot, int32_t* len, int32_t* produced, int32_t* stop
 void sprh_block_row(void* hp, int slot, int32_t* row) { static_cast<Host*>(hp)->tab.block_row(slot, row); }
 
 const char* sprh_last_error(void) { return g_err.c_str(); }
+
+// Runs the serving scheduler over a device that only records, per produced
+// token (request r's token k at out index off[r] + k): the scheduler
+// iteration (iter_out), the slot (slot_out) and the call that produced it
+// (call_out: calls are numbered from 0, prefill and decode alike), and per
+// decode call its batch size (batch_out, up to max_calls).  counters[0..4] =
+// iterations, decode steps, prefill calls, decode tokens, max batch.
+int sprh_serve(void* hp, int n, const int32_t* n_tokens, const int32_t* stop, const int32_t* arrival, int max_active,
+               int32_t* iter_out, int32_t* slot_out, int32_t* call_out, int32_t* batch_out, int max_calls,
+               int64_t* counters) {
+  Host* h = static_cast<Host*>(hp);
+  std::vector<int32_t> off(n + 1, 0);
+  int max_tok = 1;
+  for (int i = 0; i < n; ++i) {
+    off[i + 1] = off[i] + stop[i];
+    if (n_tokens[i] > max_tok) max_tok = n_tokens[i];
+  }
+  std::vector<int32_t> zeros(max_tok, 0);  // prompt ids are irrelevant to the schedule
+  std::vector<spr::ServeRequest> reqs(n);
+  for (int i = 0; i < n; ++i) reqs[i] = spr::ServeRequest{zeros.data(), n_tokens[i], stop[i], arrival[i]};
+  struct Rec : spr::ServeDevice {
+    const int32_t* off = nullptr;
+    int32_t *iter_out = nullptr, *slot_out = nullptr, *call_out = nullptr, *batch_out = nullptr;
+    int max_calls = 0, calls = 0, decodes = 0;
+    void put(int req, int k, int slot) {
+      iter_out[off[req] + k] = iteration;
+      slot_out[off[req] + k] = slot;
+      call_out[off[req] + k] = calls;
+    }
+    spr_status prefill(int m, const int32_t* slots, const int32_t* req) override {
+      for (int i = 0; i < m; ++i) put(req[i], 0, slots[i]);
+      ++calls;
+      return SPR_OK;
+    }
+    spr_status decode(int m, const int32_t* slots, const int32_t*, const int32_t* req,
+                      const int32_t* produced) override {
+      for (int i = 0; i < m; ++i) put(req[i], produced[i], slots[i]);
+      if (decodes < max_calls) batch_out[decodes] = m;
+      ++decodes;
+      ++calls;
+      return SPR_OK;
+    }
+  } rec;
+  rec.off = off.data();
+  rec.iter_out = iter_out;
+  rec.slot_out = slot_out;
+  rec.call_out = call_out;
+  rec.batch_out = batch_out;
+  rec.max_calls = max_calls;
+  spr::ServeCounters c;
+  const spr_status st = spr::serve(h->tab, h->d, n, reqs.data(), max_active, rec, &c, &g_err);
+  counters[0] = c.iterations;
+  counters[1] = c.decode_steps;
+  counters[2] = c.prefill_calls;
+  counters[3] = c.decode_tokens;
+  counters[4] = c.max_batch;
+  return st;
+}
 }

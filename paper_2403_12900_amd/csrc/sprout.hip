@@ -20,6 +20,7 @@
 //   k_row_rscale, k_tile_gemm<EpiSwiGLURows>, k_tile_gemm<EpiResidRows>;
 //   then k_gather_rows of the rows that end a prompt, and the decode LM head.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -174,6 +175,7 @@ struct RowSet {
   int pos[kRows];
   int out_row[kRows];
   int tok[kRows];
+  int hist_idx[kRows];  // token-history index of the row's token, -1 = none
 };
 
 // Launch shape of a projection, from sweeps over the 7B projection shapes on
@@ -235,7 +237,7 @@ spr_status launch_attention(spr_model* m, const AttnArgs& a) {
 // rows write their greedy token to tok_out[slot].
 template <class P, class KP>
 spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
-                   bool do_lm) {
+                   int32_t* hist) {
   const spr::Dims& d = m->d;
   Ptrs p{m->ws, &m->lay};
   const int n = rs.n;
@@ -331,7 +333,6 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e)) != SPR_OK) return st;
     }
   }
-  if (!do_lm) return SPR_OK;
   {
     EpiLogits<P> e{};
     e.n_rows = n;
@@ -350,6 +351,8 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     a.n_tiles = d.nt_lm;
     std::memcpy(a.slot, rs.slot, sizeof(a.slot));
     std::memcpy(a.out_row, rs.out_row, sizeof(a.out_row));
+    std::memcpy(a.hist_idx, rs.hist_idx, sizeof(a.hist_idx));
+    a.hist = hist;
     k_argmax_final<<<n, 256, 0, m->st>>>(a);
     SPR_LAUNCHED(m, "k_argmax_final");
   }
@@ -393,10 +396,11 @@ spr_status launch_projection(spr_model* m, int projection, int layer, int n) {
 
 // One prefill chunk: C rows (rows[] on the device), n_tiles attention query
 // tiles (ptile[] on the device), and the rows that end a prompt: emit_row[k]
-// (chunk row) emits request emit_out[k]'s first token into tok[emit_slot[k]].
+// (chunk row) emits request emit_out[k]'s first token into tok[emit_slot[k]]
+// and, when a history buffer is given, into hist[emit_hist[k]] (-1 = none).
 struct PrefillChunk {
   int C = 0, n_tiles = 0, n_emit = 0;
-  int emit_row[kRows], emit_out[kRows], emit_slot[kRows];
+  int emit_row[kRows], emit_out[kRows], emit_slot[kRows], emit_hist[kRows];
 };
 
 template <class P, class KP, int HD>
@@ -426,7 +430,7 @@ void launch_tile_gemm(hipStream_t st, const char* W, const char* X, int NT, int 
 }
 
 template <class P, class KP>
-spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits) {
+spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits, int32_t* hist) {
   const spr::Dims& d = m->d;
   Ptrs p{m->ws, &m->lay};
   using E = typename P::elem;
@@ -508,24 +512,26 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
     for (int k = 0; k < kRows; ++k) {
       a.slot[k] = k < n ? ch.emit_slot[k] : 0;
       a.out_row[k] = k < n ? ch.emit_out[k] : -1;
+      a.hist_idx[k] = k < n ? ch.emit_hist[k] : -1;
     }
+    a.hist = hist;
     k_argmax_final<<<n, 256, 0, m->st>>>(a);
     SPR_LAUNCHED(m, "k_argmax_final");
   }
   return SPR_OK;
 }
 
-spr_status prefill_any(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits) {
-  if (m->d.dtype == SPR_F32) return prefill_pass<F32, F32>(m, ch, tok, logits);
-  return m->d.kv_dtype == SPR_BF16 ? prefill_pass<BF16, BF16>(m, ch, tok, logits)
-                                   : prefill_pass<BF16, F32>(m, ch, tok, logits);
+spr_status prefill_any(spr_model* m, const PrefillChunk& ch, int32_t* tok, float* logits, int32_t* hist) {
+  if (m->d.dtype == SPR_F32) return prefill_pass<F32, F32>(m, ch, tok, logits, hist);
+  return m->d.kv_dtype == SPR_BF16 ? prefill_pass<BF16, BF16>(m, ch, tok, logits, hist)
+                                   : prefill_pass<BF16, F32>(m, ch, tok, logits, hist);
 }
 
 spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
-                       bool do_lm) {
-  if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, do_lm);
-  return m->d.kv_dtype == SPR_BF16 ? forward<BF16, BF16>(m, rs, tok_in, tok_out, logits, do_lm)
-                                   : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, do_lm);
+                       int32_t* hist) {
+  if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, hist);
+  return m->d.kv_dtype == SPR_BF16 ? forward<BF16, BF16>(m, rs, tok_in, tok_out, logits, hist)
+                                   : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, hist);
 }
 
 spr_status check_model(const spr_model* m) {
@@ -533,6 +539,109 @@ spr_status check_model(const spr_model* m) {
   if (m->sticky) return fail(SPR_ERR_HIP, "an earlier HIP error left the model unusable; release it");
   return SPR_OK;
 }
+
+// Device part of a prefill whose slots the table has already reserved:
+// uploads the slots' block-table rows, then runs the prompts (request i:
+// prompts[i][0 .. seq_lens[i])) in chunks of up to kPrefillRows rows in
+// request order; a prompt may span chunks (its later rows attend to the
+// positions an earlier chunk cached).  Request i's first token goes to
+// tok[slots[i]], its logits to row i of `logits` (if non-null), and to
+// hist[hist_idx[i]] (if hist is non-null and hist_idx[i] >= 0).  The host
+// tables stay alive until the final synchronize.
+spr_status prefill_device(spr_model* m, int n, const int32_t* slots, const int32_t* const* prompts,
+                          const int32_t* seq_lens, int32_t* tok, float* logits, int32_t* hist,
+                          const int32_t* hist_idx) {
+  Ptrs p{m->ws, &m->lay};
+  spr_status st;
+  std::vector<int32_t> rows(static_cast<size_t>(n) * m->d.mb);
+  for (int i = 0; i < n; ++i) m->tab.block_row(slots[i], rows.data() + static_cast<size_t>(i) * m->d.mb);
+  for (int i = 0; i < n; ++i)
+    SPR_HIP(m, hipMemcpyAsync(p.bt() + static_cast<size_t>(slots[i]) * m->d.mb,
+                              rows.data() + static_cast<size_t>(i) * m->d.mb, m->d.mb * sizeof(int32_t),
+                              hipMemcpyHostToDevice, m->st));
+  std::vector<std::vector<PrefillRow>> row_tabs;
+  std::vector<std::vector<PrefillTile>> tile_tabs;
+  PrefillChunk ch;
+  std::vector<PrefillRow> chunk_rows;
+  std::vector<PrefillTile> tiles;
+  auto flush = [&]() -> spr_status {
+    if (chunk_rows.empty()) return SPR_OK;
+    ch.C = static_cast<int>(chunk_rows.size());
+    ch.n_tiles = static_cast<int>(tiles.size());
+    if (ch.n_tiles > spr::kPrefillTiles) return fail(SPR_ERR_INVALID_ARG, "internal: prefill tile table overflow");
+    row_tabs.push_back(std::move(chunk_rows));
+    tile_tabs.push_back(std::move(tiles));
+    chunk_rows = {};
+    tiles = {};
+    SPR_HIP(m, hipMemcpyAsync(p.prow(), row_tabs.back().data(), row_tabs.back().size() * sizeof(PrefillRow),
+                              hipMemcpyHostToDevice, m->st));
+    SPR_HIP(m, hipMemcpyAsync(p.ptile(), tile_tabs.back().data(), tile_tabs.back().size() * sizeof(PrefillTile),
+                              hipMemcpyHostToDevice, m->st));
+    spr_status s2 = prefill_any(m, ch, tok, logits, hist);
+    ch = PrefillChunk{};
+    return s2;
+  };
+  for (int i = 0; i < n; ++i) {
+    int pos = 0;
+    while (pos < seq_lens[i]) {
+      if (static_cast<int>(chunk_rows.size()) == spr::kPrefillRows) {
+        if ((st = flush()) != SPR_OK) return st;
+      }
+      // The next segment of request i that fits this chunk, in query tiles of 16.
+      const int seg = std::min(seq_lens[i] - pos, spr::kPrefillRows - static_cast<int>(chunk_rows.size()));
+      const int row0 = static_cast<int>(chunk_rows.size());
+      for (int k = 0; k < seg; ++k) chunk_rows.push_back(PrefillRow{slots[i], pos + k, prompts[i][pos + k], 0});
+      for (int k = 0; k < seg; k += 16) tiles.push_back(PrefillTile{slots[i], row0 + k, std::min(16, seg - k), pos + k});
+      pos += seg;
+      if (pos == seq_lens[i]) {
+        ch.emit_row[ch.n_emit] = row0 + seg - 1;
+        ch.emit_out[ch.n_emit] = i;
+        ch.emit_slot[ch.n_emit] = slots[i];
+        ch.emit_hist[ch.n_emit] = hist != nullptr && hist_idx != nullptr ? hist_idx[i] : -1;
+        ++ch.n_emit;
+      }
+    }
+  }
+  if ((st = flush()) != SPR_OK) return st;
+  SPR_HIP(m, hipStreamSynchronize(m->st));
+  return SPR_OK;
+}
+
+// Device side of spr_serve: runs the scheduler's prefill and decode calls on
+// the kernels above; request r's token k lands in out[off[r] + k].
+struct GpuServe : spr::ServeDevice {
+  spr_model* m = nullptr;
+  const spr::ServeRequest* reqs = nullptr;
+  const int64_t* off = nullptr;
+  int32_t* tok = nullptr;
+  int32_t* out = nullptr;
+
+  spr_status prefill(int n, const int32_t* slots, const int32_t* req) override {
+    std::vector<const int32_t*> prompts(n);
+    std::vector<int32_t> lens(n), hidx(n);
+    for (int i = 0; i < n; ++i) {
+      prompts[i] = reqs[req[i]].tokens;
+      lens[i] = reqs[req[i]].n_tokens;
+      hidx[i] = static_cast<int32_t>(off[req[i]]);
+    }
+    return prefill_device(m, n, slots, prompts.data(), lens.data(), tok, nullptr, out, hidx.data());
+  }
+
+  spr_status decode(int n, const int32_t* slots, const int32_t* lens, const int32_t* req,
+                    const int32_t* produced) override {
+    RowSet rs;
+    rs.n = n;
+    for (int r = 0; r < kRows; ++r) {
+      const bool v = r < n;
+      rs.slot[r] = v ? slots[r] : 0;
+      rs.pos[r] = v ? lens[r] : 0;
+      rs.out_row[r] = v ? r : -1;
+      rs.tok[r] = 0;
+      rs.hist_idx[r] = v ? static_cast<int>(off[req[r]] + produced[r]) : -1;
+    }
+    return forward_any(m, rs, tok, tok, nullptr, out);
+  }
+};
 
 }  // namespace
 
@@ -613,64 +722,13 @@ spr_status spr_prefill(spr_model* m, int32_t n, const int32_t* slots, const int3
     if (tokens[t] < 0 || tokens[t] >= m->d.V) return fail(SPR_ERR_INVALID_ARG, "prefill: token id out of range");
 
   m->tab.commit_prefill(n, slots, seq_lens, stop_lens, retired);
-  Ptrs p{m->ws, &m->lay};
-  std::vector<int32_t> rows(static_cast<size_t>(n) * m->d.mb);
-  for (int i = 0; i < n; ++i) m->tab.block_row(slots[i], rows.data() + static_cast<size_t>(i) * m->d.mb);
-  for (int i = 0; i < n; ++i)
-    SPR_HIP(m, hipMemcpyAsync(p.bt() + static_cast<size_t>(slots[i]) * m->d.mb,
-                              rows.data() + static_cast<size_t>(i) * m->d.mb, m->d.mb * sizeof(int32_t),
-                              hipMemcpyHostToDevice, m->st));
-  SPR_HIP(m, hipStreamSynchronize(m->st));
-
-  // Chunks of up to kPrefillRows rows in request order; a prompt may span
-  // chunks (its later rows attend to the positions an earlier chunk cached).
-  // The host tables of every chunk stay alive until the final synchronize.
-  std::vector<std::vector<PrefillRow>> row_tabs;
-  std::vector<std::vector<PrefillTile>> tile_tabs;
-  PrefillChunk ch;
-  std::vector<PrefillRow> chunk_rows;
-  std::vector<PrefillTile> tiles;
-  auto flush = [&]() -> spr_status {
-    if (chunk_rows.empty()) return SPR_OK;
-    ch.C = static_cast<int>(chunk_rows.size());
-    ch.n_tiles = static_cast<int>(tiles.size());
-    if (ch.n_tiles > spr::kPrefillTiles) return fail(SPR_ERR_INVALID_ARG, "internal: prefill tile table overflow");
-    row_tabs.push_back(std::move(chunk_rows));
-    tile_tabs.push_back(std::move(tiles));
-    chunk_rows = {};
-    tiles = {};
-    SPR_HIP(m, hipMemcpyAsync(p.prow(), row_tabs.back().data(), row_tabs.back().size() * sizeof(PrefillRow),
-                              hipMemcpyHostToDevice, m->st));
-    SPR_HIP(m, hipMemcpyAsync(p.ptile(), tile_tabs.back().data(), tile_tabs.back().size() * sizeof(PrefillTile),
-                              hipMemcpyHostToDevice, m->st));
-    spr_status s2 = prefill_any(m, ch, tok, logits);
-    ch = PrefillChunk{};
-    return s2;
-  };
+  std::vector<const int32_t*> prompts(n);
   int64_t t = 0;
   for (int i = 0; i < n; ++i) {
-    int pos = 0;
-    while (pos < seq_lens[i]) {
-      if (static_cast<int>(chunk_rows.size()) == spr::kPrefillRows) {
-        if ((st = flush()) != SPR_OK) return st;
-      }
-      // The next segment of request i that fits this chunk, in query tiles of 16.
-      const int seg = std::min(seq_lens[i] - pos, spr::kPrefillRows - static_cast<int>(chunk_rows.size()));
-      const int row0 = static_cast<int>(chunk_rows.size());
-      for (int k = 0; k < seg; ++k, ++t) chunk_rows.push_back(PrefillRow{slots[i], pos + k, tokens[t], 0});
-      for (int k = 0; k < seg; k += 16) tiles.push_back(PrefillTile{slots[i], row0 + k, std::min(16, seg - k), pos + k});
-      pos += seg;
-      if (pos == seq_lens[i]) {
-        ch.emit_row[ch.n_emit] = row0 + seg - 1;
-        ch.emit_out[ch.n_emit] = i;
-        ch.emit_slot[ch.n_emit] = slots[i];
-        ++ch.n_emit;
-      }
-    }
+    prompts[i] = tokens + t;
+    t += seq_lens[i];
   }
-  if ((st = flush()) != SPR_OK) return st;
-  SPR_HIP(m, hipStreamSynchronize(m->st));
-  return SPR_OK;
+  return prefill_device(m, n, slots, prompts.data(), seq_lens, tok, logits, nullptr, nullptr);
 }
 
 spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots, const int32_t* lens, int32_t* tok,
@@ -690,8 +748,9 @@ spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots,
     rs.pos[r] = v ? lens[r] : 0;
     rs.out_row[r] = v ? r : -1;
     rs.tok[r] = 0;
+    rs.hist_idx[r] = -1;
   }
-  if ((st = forward_any(m, rs, tok, tok, logits, true)) != SPR_OK) return st;
+  if ((st = forward_any(m, rs, tok, tok, logits, nullptr)) != SPR_OK) return st;
   m->tab.commit_decode(n_active, slots, retired);
   return SPR_OK;
 }
@@ -809,6 +868,42 @@ spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows,
   if (st != SPR_OK) return st;
   if (e != hipSuccess) return hip_fail(m, "time_projection", e);
   *avg_us = 1000.f * ms / static_cast<float>(reps);
+  return SPR_OK;
+}
+
+spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t* tok,
+                     int32_t* out, spr_serve_stats* stats) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (n < 0 || (n > 0 && (reqs == nullptr || tok == nullptr || out == nullptr)))
+    return fail(SPR_ERR_INVALID_ARG, "serve: n must be >= 0, and reqs, tok and out non-null");
+  std::vector<spr::ServeRequest> rq(n);
+  std::vector<int64_t> off(static_cast<size_t>(n) + 1, 0);
+  for (int i = 0; i < n; ++i) {
+    rq[i] = spr::ServeRequest{reqs[i].tokens, reqs[i].n_tokens, reqs[i].stop_len, reqs[i].arrival};
+    off[i + 1] = off[i] + std::max(reqs[i].stop_len, 0);
+  }
+  if (off[n] > INT32_MAX) return fail(SPR_ERR_INVALID_ARG, "serve: too many output tokens");
+  GpuServe dev;
+  dev.m = m;
+  dev.reqs = rq.data();
+  dev.off = off.data();
+  dev.tok = tok;
+  dev.out = out;
+  spr::ServeCounters c;
+  std::string err;
+  st = spr::serve(m->tab, m->d, n, rq.data(), max_active, dev, &c, &err);
+  if (st != SPR_OK) return err.empty() ? st : fail(st, err);
+  SPR_HIP(m, hipStreamSynchronize(m->st));
+  if (stats != nullptr) {
+    stats->iterations = c.iterations;
+    stats->decode_steps = c.decode_steps;
+    stats->prefill_calls = c.prefill_calls;
+    stats->decode_tokens = c.decode_tokens;
+    stats->max_batch = c.max_batch;
+    stats->mean_batch = c.mean_batch;
+  }
   return SPR_OK;
 }
 

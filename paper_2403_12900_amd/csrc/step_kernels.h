@@ -34,9 +34,11 @@ __global__ __launch_bounds__(64) void k_embed(EmbedArgs a) {
 struct ArgmaxArgs {
   const float2* part;       // [tiles][kRows] (value, index bits)
   int32_t* tok_dev;         // written at the row's slot
+  int32_t* hist;            // or null: token history, written at hist_idx[row] when >= 0
   int n_tiles;
   int slot[kRows];
   int out_row[kRows];       // -1: row emits no token
+  int hist_idx[kRows];
 };
 
 __device__ __forceinline__ void better_of(float& v, int& i, float ov, int oi) {
@@ -67,6 +69,7 @@ __global__ __launch_bounds__(256) void k_argmax_final(ArgmaxArgs a) {
   if (threadIdx.x == 0) {
     for (int w = 1; w < 4; ++w) better_of(v, idx, sv[w], si[w]);
     a.tok_dev[a.slot[b]] = idx;
+    if (a.hist != nullptr && a.hist_idx[b] >= 0) a.hist[a.hist_idx[b]] = idx;
   }
 }
 
