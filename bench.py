@@ -21,6 +21,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -175,6 +177,56 @@ def time_prefill(model, m, wl, stops, reps: int = 3):
             "peak_tflops": PEAK_BF16_TFLOPS, "mfma_frac": round(tflops * issue / PEAK_BF16_TFLOPS, 4)}
 
 
+def time_serving(cfg, n_req: int = 96, max_active: int = 32):
+    """Continuous batching (spr_serve) against closed batches, on the same
+    requests: n_req requests drawn with the workload's recipe, all waiting at
+    the start, at most max_active in flight.  Closed batches take max_active
+    requests at a time and drain each batch before the next starts; continuous
+    batching refills a slot as soon as its request retires.  Both include
+    prefill.  Tokens = every generated token (the prefill's first ones too)."""
+    import dataclasses
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.workload import make_workload
+    m = cfg.model
+    c2 = dataclasses.replace(cfg, workload=dataclasses.replace(cfg.workload, batch=n_req))
+    wl = make_workload(c2, seed=cfg.workload_seed + 7919)
+    prompts = [np.asarray(t) for t in wl.tokens]
+    stops = [int(x) for x in wl.stop_lens]
+    need = sorted(((len(p) + s - 1 + 15) // 16 for p, s in zip(prompts, stops)), reverse=True)
+    max_ctx = max(len(p) + s - 1 for p, s in zip(prompts, stops))
+    model = DecodeModel(m, cfg.weight_seed, max_slots=max_active, max_ctx=max_ctx, kv_blocks=sum(need[:max_active]))
+    model.serve(prompts[:4], [min(s, 4) for s in stops[:4]], max_active)          # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, st = model.serve(prompts, stops, max_active)
+    cont = time.perf_counter() - t0
+    tok = model.new_token_buffer()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for b0 in range(0, n_req, max_active):
+        idx = list(range(b0, min(n_req, b0 + max_active)))
+        slots = list(range(len(idx)))
+        _, retired = model.prefill(slots, [prompts[i] for i in idx], [stops[i] for i in idx], tok)
+        lens = [len(prompts[i]) for i in idx]
+        active = [k for k in slots if not retired[k]]
+        while active:
+            _, r = model.decode_step(active, [lens[k] for k in active], tok)
+            for k in active:
+                lens[k] += 1
+            active = [k for j, k in enumerate(active) if not r[j]]
+        for k in slots:
+            model.free_slot(k)
+    torch.cuda.synchronize()
+    closed = time.perf_counter() - t0
+    model.close()
+    total = sum(stops)
+    return {"requests": n_req, "max_active": max_active, "generated_tokens": total,
+            "continuous_tokens_per_s": round(total / cont, 1), "closed_batches_tokens_per_s": round(total / closed, 1),
+            "continuous_s": round(cont, 3), "closed_batches_s": round(closed, 3),
+            "continuous_mean_batch": round(st["mean_batch"], 2), "continuous_decode_steps": st["decode_steps"]}
+
+
 def cpu_baseline(cfg, wl, seconds: float):
     """The CPU oracle's KV-cache decode step on the same workload, bounded sample."""
     import numpy as np
@@ -221,6 +273,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-serving", action="store_true", help="skip the continuous-batching measurement")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only launch the dominant kernel and a calibration copy (for rocprofv3 --pmc)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -336,6 +389,10 @@ def main():
     model.close()
     del model
     torch.cuda.empty_cache()
+    if not args.no_serving:
+        out["serving"] = time_serving(cfg)
+        log(f"serving: {out['serving']}")
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_seconds)
         log(f"cpu baseline: {out['cpu_baseline']}")
