@@ -199,7 +199,8 @@ def time_serving(cfg, n_req: int = 96, max_active: int = 32):
     model.serve(prompts[:4], [min(s, 4) for s in stops[:4]], max_active)          # warm-up
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    _, st = model.serve(prompts, stops, max_active)
+    n_lv = len(cfg.workload.prefix_lens)
+    _, st = model.serve(prompts, stops, max_active, levels=[int(x) for x in wl.levels])
     cont = time.perf_counter() - t0
     tok = model.new_token_buffer()
     torch.cuda.synchronize()
@@ -224,7 +225,12 @@ def time_serving(cfg, n_req: int = 96, max_active: int = 32):
     return {"requests": n_req, "max_active": max_active, "generated_tokens": total,
             "continuous_tokens_per_s": round(total / cont, 1), "closed_batches_tokens_per_s": round(total / closed, 1),
             "continuous_s": round(cont, 3), "closed_batches_s": round(closed, 3),
-            "continuous_mean_batch": round(st["mean_batch"], 2), "continuous_decode_steps": st["decode_steps"]}
+            "continuous_mean_batch": round(st["mean_batch"], 2), "continuous_decode_steps": st["decode_steps"],
+            # Eq. 2's per-level p: mean device seconds per request of each directive level, each
+            # iteration's time shared equally by the requests it served.
+            "level_requests": st["level_requests"][:n_lv],
+            "level_mean_tokens": [round(x, 1) for x in st["level_tokens"][:n_lv]],
+            "level_seconds_per_request": [round(x, 4) for x in st["level_seconds"][:n_lv]]}
 
 
 def cpu_baseline(cfg, wl, seconds: float):

@@ -178,21 +178,31 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
  */
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
 
+#define SPR_MAX_LEVELS 8 /* directive levels a serving run can profile */
+
 /* One request of a serving run (host memory, read during the call). */
 typedef struct {
   const int32_t* tokens; /* prompt: directive prefix followed by the user prompt */
   int32_t n_tokens;      /* >= 1 */
-  int32_t stop_len;      /* tokens to generate, >= 1; n_tokens + stop_len - 1 <= max_ctx */
+  int32_t stop_len;      /* generation limit, >= 1; n_tokens + stop_len - 1 <= max_ctx */
   int32_t arrival;       /* first scheduler iteration it may be admitted in (0 = at once) */
+  int32_t level;         /* directive level (Definition 1), 0..SPR_MAX_LEVELS-1; profiling tag only */
 } spr_request;
 
 typedef struct {
   int64_t iterations;    /* scheduler iterations run */
   int64_t decode_steps;  /* decode steps launched */
   int64_t prefill_calls; /* batched prefills launched */
-  int64_t decode_tokens; /* tokens produced by decode steps */
+  int64_t decode_tokens; /* decode rows launched (tokens past an EOS included) */
   int32_t max_batch;     /* largest decode batch */
   double mean_batch;     /* mean decode batch */
+  double device_seconds; /* device time from the call's first work to its last iteration */
+  /* Per directive level, the profiles Eq. 2 consumes (p: processing time per
+     request).  Each iteration's device time is shared equally by the
+     requests it served; a request's time is the sum of its shares. */
+  int32_t level_requests[SPR_MAX_LEVELS]; /* requests of the level */
+  double level_tokens[SPR_MAX_LEVELS];    /* mean generated tokens (lengths) per request */
+  double level_seconds[SPR_MAX_LEVELS];   /* p: mean device seconds per request */
 } spr_serve_stats;
 
 /*
@@ -207,21 +217,31 @@ typedef struct {
  *   2. prefills the admitted requests together (first tokens);
  *   3. runs one decode step over every request still generating;
  *   4. retires requests that reached their stop length, freeing their slots
- *      and KV blocks for the next iteration.
+ *      and KV blocks for the next iteration;
+ *   5. retires requests whose previous-iteration token was eos_id (Section
+ *      II-A: generation ends at EOS or at the preset limit).  The tokens are
+ *      read back one iteration late, so the host never waits for the
+ *      iteration it has just enqueued; such a request runs one more decode
+ *      row (two if EOS was its prefill token), whose token is discarded.
  * Iterations with nothing in flight skip to the next arrival.  Outputs are
- * the same greedy tokens each request would get served alone.
+ * the greedy tokens each request would get served alone.
  *   max_active 1..max_slots
+ *   eos_id     token id that ends a request, or negative for none
  *   tok        device int32 [max_slots]: scratch token buffer, indexed by slot
  *   out        device int32 [sum of stop_len]: request i's tokens at offset
- *              stop_len[0] + ... + stop_len[i-1]
+ *              stop_len[0] + ... + stop_len[i-1]; entries past its length
+ *              are unspecified
+ *   lengths    host int32 [n] or NULL: tokens generated per request, up to
+ *              and including the first EOS, else stop_len
  *   stats      host, or NULL
  * Needs every slot free on entry (SPR_ERR_STATE otherwise) and leaves them
  * free.  A malformed request, or one that max_ctx or the KV pool could never
  * hold, fails with SPR_ERR_INVALID_ARG before any work is enqueued.
- * Synchronous: out is complete when it returns.
+ * Synchronous: out is complete when it returns.  Uses a few HIP events and,
+ * with an EOS id, 16 * max_slots bytes of pinned host memory for the call.
  */
-spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t* tok,
-                     int32_t* out, spr_serve_stats* stats);
+spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t eos_id,
+                     int32_t* tok, int32_t* out, int32_t* lengths, spr_serve_stats* stats);
 
 /* Releases the host state.  The workspace is the caller's to free afterwards. */
 spr_status spr_release(spr_model* m);

@@ -41,14 +41,19 @@ _I32P = ctypes.POINTER(ctypes.c_int32)
 _lib = None
 
 
+MAX_LEVELS = 8  # SPR_MAX_LEVELS
+
+
 class SprRequest(ctypes.Structure):
     _fields_ = [("tokens", _I32P), ("n_tokens", ctypes.c_int32), ("stop_len", ctypes.c_int32),
-                ("arrival", ctypes.c_int32)]
+                ("arrival", ctypes.c_int32), ("level", ctypes.c_int32)]
 
 
 class SprServeStats(ctypes.Structure):
     _fields_ = [("iterations", ctypes.c_int64), ("decode_steps", ctypes.c_int64), ("prefill_calls", ctypes.c_int64),
-                ("decode_tokens", ctypes.c_int64), ("max_batch", ctypes.c_int32), ("mean_batch", ctypes.c_double)]
+                ("decode_tokens", ctypes.c_int64), ("max_batch", ctypes.c_int32), ("mean_batch", ctypes.c_double),
+                ("device_seconds", ctypes.c_double), ("level_requests", ctypes.c_int32 * MAX_LEVELS),
+                ("level_tokens", ctypes.c_double * MAX_LEVELS), ("level_seconds", ctypes.c_double * MAX_LEVELS)]
 
 
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -82,8 +87,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_float)]
     L.spr_serve.restype = ctypes.c_int
-    L.spr_serve.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(SprRequest), ctypes.c_int32, vp, vp,
-                            ctypes.POINTER(SprServeStats)]
+    L.spr_serve.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(SprRequest), ctypes.c_int32, ctypes.c_int32, vp, vp,
+                            _I32P, ctypes.POINTER(SprServeStats)]
     L.spr_release.restype = ctypes.c_int
     L.spr_release.argtypes = [vp]
     L.spr_last_error.restype = ctypes.c_char_p
@@ -197,24 +202,32 @@ class DecodeModel:
         return float(out.value)
 
     def serve(self, prompts: Sequence[Sequence[int]], stop_lens: Sequence[int], max_active: int,
-              arrivals: Optional[Sequence[int]] = None):
-        """Continuous batching of all requests (spr_serve); returns (tokens per request, stats dict)."""
+              arrivals: Optional[Sequence[int]] = None, levels: Optional[Sequence[int]] = None, eos_id: int = -1):
+        """Continuous batching of all requests (spr_serve).
+
+        Returns (tokens per request, each cut to its length; stats dict with
+        per-level lists for the level_* entries)."""
         n = len(prompts)
         arrivals = [0] * n if arrivals is None else list(arrivals)
+        levels = [0] * n if levels is None else list(levels)
         keep = [_i32(p) for p in prompts]
         reqs = (SprRequest * max(n, 1))()
         for i in range(n):
-            reqs[i] = SprRequest(_ptr(keep[i]), len(keep[i]), int(stop_lens[i]), int(arrivals[i]))
+            reqs[i] = SprRequest(_ptr(keep[i]), len(keep[i]), int(stop_lens[i]), int(arrivals[i]), int(levels[i]))
         total = int(sum(stop_lens))
         out = self.torch.full((max(total, 1),), -1, dtype=self.torch.int32, device=self.device)
         tok = self.new_token_buffer()
+        lengths = np.zeros(max(n, 1), dtype=np.int32)
         st = SprServeStats()
-        _check(self.lib.spr_serve(self.h, n, reqs, max_active, ctypes.c_void_p(tok.data_ptr()),
-                                  ctypes.c_void_p(out.data_ptr()), ctypes.byref(st)))
+        _check(self.lib.spr_serve(self.h, n, reqs, max_active, int(eos_id), ctypes.c_void_p(tok.data_ptr()),
+                                  ctypes.c_void_p(out.data_ptr()), _ptr(lengths), ctypes.byref(st)))
         flat = out.cpu().numpy()
         off = np.concatenate([[0], np.cumsum(np.asarray(stop_lens, dtype=np.int64))]).astype(int)
-        toks = [flat[off[i]:off[i + 1]].copy() for i in range(n)]
-        stats = {f: getattr(st, f) for f, _ in SprServeStats._fields_}
+        toks = [flat[off[i]:off[i] + lengths[i]].copy() for i in range(n)]
+        stats = {}
+        for f, _ in SprServeStats._fields_:
+            v = getattr(st, f)
+            stats[f] = list(v) if f.startswith("level_") else v
         return toks, stats
 
     def close(self):

@@ -1,6 +1,8 @@
 // Host-side bookkeeping of the decode model (see host_state.h).
 #include "host_state.h"
 
+#include <utility>
+
 #include <cmath>
 #include <limits>
 
@@ -276,7 +278,7 @@ void SlotTable::block_row(int slot, int32_t* row) const {
 }
 
 spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs, int max_active, ServeDevice& dev,
-                 ServeCounters* counters, std::string* err) {
+                 ServeCounters* counters, std::vector<int32_t>* lengths, std::string* err) {
   if (n < 0 || (n > 0 && reqs == nullptr)) {
     *err = "serve: n must be >= 0 and requests non-null";
     return SPR_ERR_INVALID_ARG;
@@ -314,6 +316,23 @@ spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs,
   };
   std::vector<Live> live;
   std::vector<char> busy(d.S, 0);
+  std::vector<int32_t> length(n);
+  for (int i = 0; i < n; ++i) length[i] = reqs[i].stop_len;
+  std::vector<std::pair<int, int>> eos;
+  auto note_eos = [&]() {  // record EOS lengths; retire requests still in flight
+    for (const auto& e : eos) {
+      if (e.second + 1 < length[e.first]) length[e.first] = e.second + 1;
+      for (size_t i = 0; i < live.size(); ++i) {
+        if (live[i].req == e.first) {
+          tab.commit_free(live[i].slot);
+          busy[live[i].slot] = 0;
+          live.erase(live.begin() + static_cast<std::ptrdiff_t>(i));
+          break;
+        }
+      }
+    }
+    eos.clear();
+  };
   ServeCounters c;
   int64_t batch_sum = 0;
   int q = 0;
@@ -394,12 +413,19 @@ spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs,
       }
       live.swap(keep);
     }
+    spr_status st = dev.end_iteration(false, &eos);
+    if (st != SPR_OK) return st;
+    note_eos();
     ++c.iterations;
     ++it;
     if (live.empty() && q < n && reqs[q].arrival > it) it = reqs[q].arrival;  // idle until the next arrival
   }
+  spr_status st = dev.end_iteration(true, &eos);
+  if (st != SPR_OK) return st;
+  note_eos();
   c.mean_batch = c.decode_steps > 0 ? static_cast<double>(batch_sum) / c.decode_steps : 0.0;
   if (counters) *counters = c;
+  if (lengths) *lengths = length;
   return SPR_OK;
 }
 

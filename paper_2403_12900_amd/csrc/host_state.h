@@ -7,6 +7,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/sprout.h"
@@ -94,7 +95,12 @@ class SlotTable {
 //   2. prefills the admitted requests together (each emits its first token);
 //   3. runs one decode step over every request still generating;
 //   4. retires requests that produced their stop length and frees their slots
-//      and blocks at once, for the next iteration's admissions.
+//      and blocks at once, for the next iteration's admissions;
+//   5. retires requests whose token in the previous iteration was the EOS id
+//      (Section II-A: generation ends at EOS or at the preset limit).  The
+//      device reports EOS one iteration late, so the host never waits for the
+//      iteration it has just enqueued; such a request runs one extra decode
+//      row, inside the KV blocks it reserved, whose token is discarded.
 // Iterations with nothing in flight jump to the next arrival.  The device
 // work goes through ServeDevice, so the policy runs unchanged on the host
 // alone (tests) or over the GPU kernels (spr_serve).
@@ -122,12 +128,18 @@ class ServeDevice {
   // token the step produces for it.
   virtual spr_status decode(int n, const int32_t* slots, const int32_t* lens, const int32_t* req,
                             const int32_t* produced) = 0;
+  // Called after each iteration's device work.  Appends to *eos the (request,
+  // token index) pairs whose token was the EOS id in the previous iteration;
+  // with final = true (once, after the last iteration), in the last one too.
+  virtual spr_status end_iteration(bool final, std::vector<std::pair<int, int>>* eos) = 0;
 };
 
 // Runs the whole request list.  Needs every slot free on entry; leaves every
 // slot free on success.  SPR_ERR_INVALID_ARG for a malformed request or one
 // the KV pool could never hold; errors of the device calls are returned as is.
+// lengths (may be null) receives each request's generated tokens: up to and
+// including its first EOS, else its stop length.
 spr_status serve(SlotTable& tab, const Dims& d, int n, const ServeRequest* reqs, int max_active, ServeDevice& dev,
-                 ServeCounters* counters, std::string* err);
+                 ServeCounters* counters, std::vector<int32_t>* lengths, std::string* err);
 
 }  // namespace spr

@@ -89,11 +89,14 @@ const char* sprh_last_error(void) { return g_err.c_str(); }
 // token (request r's token k at out index off[r] + k): the scheduler
 // iteration (iter_out), the slot (slot_out) and the call that produced it
 // (call_out: calls are numbered from 0, prefill and decode alike), and per
-// decode call its batch size (batch_out, up to max_calls).  counters[0..4] =
-// iterations, decode steps, prefill calls, decode tokens, max batch.
+// decode call its batch size (batch_out, up to max_calls).  Token k of
+// request eos_req[j] is taken to be the EOS id when k == eos_idx[j]
+// (j < n_eos).  lengths_out[r] receives the scheduler's length of request r.
+// counters[0..4] = iterations, decode steps, prefill calls, decode tokens,
+// max batch.
 int sprh_serve(void* hp, int n, const int32_t* n_tokens, const int32_t* stop, const int32_t* arrival, int max_active,
-               int32_t* iter_out, int32_t* slot_out, int32_t* call_out, int32_t* batch_out, int max_calls,
-               int64_t* counters) {
+               int n_eos, const int32_t* eos_req, const int32_t* eos_idx, int32_t* iter_out, int32_t* slot_out,
+               int32_t* call_out, int32_t* batch_out, int max_calls, int32_t* lengths_out, int64_t* counters) {
   Host* h = static_cast<Host*>(hp);
   std::vector<int32_t> off(n + 1, 0);
   int max_tok = 1;
@@ -108,10 +111,27 @@ int sprh_serve(void* hp, int n, const int32_t* n_tokens, const int32_t* stop, co
     const int32_t* off = nullptr;
     int32_t *iter_out = nullptr, *slot_out = nullptr, *call_out = nullptr, *batch_out = nullptr;
     int max_calls = 0, calls = 0, decodes = 0;
+    std::vector<std::pair<int, int>> eos_set, cur, prev;
     void put(int req, int k, int slot) {
       iter_out[off[req] + k] = iteration;
       slot_out[off[req] + k] = slot;
       call_out[off[req] + k] = calls;
+      cur.emplace_back(req, k);
+    }
+    void hits(const std::vector<std::pair<int, int>>& v, std::vector<std::pair<int, int>>* eos) const {
+      for (const auto& t : v)
+        for (const auto& e : eos_set)
+          if (e == t) eos->push_back(t);
+    }
+    spr_status end_iteration(bool final, std::vector<std::pair<int, int>>* eos) override {
+      hits(prev, eos);
+      if (final) {
+        hits(cur, eos);
+        cur.clear();
+      }
+      prev.swap(cur);
+      cur.clear();
+      return SPR_OK;
     }
     spr_status prefill(int m, const int32_t* slots, const int32_t* req) override {
       for (int i = 0; i < m; ++i) put(req[i], 0, slots[i]);
@@ -133,8 +153,11 @@ int sprh_serve(void* hp, int n, const int32_t* n_tokens, const int32_t* stop, co
   rec.call_out = call_out;
   rec.batch_out = batch_out;
   rec.max_calls = max_calls;
+  for (int j = 0; j < n_eos; ++j) rec.eos_set.emplace_back(eos_req[j], eos_idx[j]);
   spr::ServeCounters c;
-  const spr_status st = spr::serve(h->tab, h->d, n, reqs.data(), max_active, rec, &c, &g_err);
+  std::vector<int32_t> lengths;
+  const spr_status st = spr::serve(h->tab, h->d, n, reqs.data(), max_active, rec, &c, &lengths, &g_err);
+  for (int i = 0; i < n && st == SPR_OK; ++i) lengths_out[i] = lengths[i];
   counters[0] = c.iterations;
   counters[1] = c.decode_steps;
   counters[2] = c.prefill_calls;

@@ -608,13 +608,36 @@ spr_status prefill_device(spr_model* m, int n, const int32_t* slots, const int32
 }
 
 // Device side of spr_serve: runs the scheduler's prefill and decode calls on
-// the kernels above; request r's token k lands in out[off[r] + k].
+// the kernels above; request r's token k lands in out[off[r] + k].  With an
+// EOS id, each call's tokens (the slot-indexed token buffer) are copied
+// asynchronously into pinned host memory, and end_iteration reads the
+// previous iteration's copies, so the host waits only for work that finished
+// while the current iteration runs.  An event closes every iteration; each
+// iteration's device time is later shared equally by the requests it served.
 struct GpuServe : spr::ServeDevice {
   spr_model* m = nullptr;
   const spr::ServeRequest* reqs = nullptr;
   const int64_t* off = nullptr;
   int32_t* tok = nullptr;
   int32_t* out = nullptr;
+  int eos_id = -1;
+  int32_t* pin = nullptr;             // pinned [2 parities][2 phases][max_slots]
+  hipEvent_t snap[2] = {nullptr, nullptr};
+  struct Row {
+    int slot, req, idx;
+  };
+  std::vector<Row> rows[2][2];        // [parity][0 prefill, 1 decode]
+  bool pending = false;               // the previous iteration has copies to read
+  int par = 0;
+  std::vector<hipEvent_t> ev_iter;    // end of each iteration
+  std::vector<std::vector<int>> served;  // requests each iteration served
+  std::vector<int> cur;
+
+  spr_status snapshot(int phase) {
+    SPR_HIP(m, hipMemcpyAsync(pin + (par * 2 + phase) * m->d.S, tok, m->d.S * sizeof(int32_t),
+                              hipMemcpyDeviceToHost, m->st));
+    return SPR_OK;
+  }
 
   spr_status prefill(int n, const int32_t* slots, const int32_t* req) override {
     std::vector<const int32_t*> prompts(n);
@@ -623,8 +646,12 @@ struct GpuServe : spr::ServeDevice {
       prompts[i] = reqs[req[i]].tokens;
       lens[i] = reqs[req[i]].n_tokens;
       hidx[i] = static_cast<int32_t>(off[req[i]]);
+      cur.push_back(req[i]);
     }
-    return prefill_device(m, n, slots, prompts.data(), lens.data(), tok, nullptr, out, hidx.data());
+    spr_status st = prefill_device(m, n, slots, prompts.data(), lens.data(), tok, nullptr, out, hidx.data());
+    if (st != SPR_OK || eos_id < 0) return st;
+    for (int i = 0; i < n; ++i) rows[par][0].push_back(Row{slots[i], req[i], 0});
+    return snapshot(0);
   }
 
   spr_status decode(int n, const int32_t* slots, const int32_t* lens, const int32_t* req,
@@ -639,9 +666,47 @@ struct GpuServe : spr::ServeDevice {
       rs.tok[r] = 0;
       rs.hist_idx[r] = v ? static_cast<int>(off[req[r]] + produced[r]) : -1;
     }
-    return forward_any(m, rs, tok, tok, nullptr, out);
+    for (int i = 0; i < n; ++i) cur.push_back(req[i]);
+    spr_status st = forward_any(m, rs, tok, tok, nullptr, out);
+    if (st != SPR_OK || eos_id < 0) return st;
+    for (int i = 0; i < n; ++i) rows[par][1].push_back(Row{slots[i], req[i], produced[i]});
+    return snapshot(1);
+  }
+
+  // Appends the EOS hits among the copies of parity q (already complete).
+  void scan(int q, std::vector<std::pair<int, int>>* eos) {
+    for (int ph = 0; ph < 2; ++ph) {
+      for (const Row& r : rows[q][ph])
+        if (pin[(q * 2 + ph) * m->d.S + r.slot] == eos_id) eos->emplace_back(r.req, r.idx);
+      rows[q][ph].clear();
+    }
+  }
+
+  spr_status end_iteration(bool final, std::vector<std::pair<int, int>>* eos) override {
+    hipEvent_t e = nullptr;
+    SPR_HIP(m, hipEventCreate(&e));
+    ev_iter.push_back(e);
+    served.push_back(std::move(cur));
+    cur.clear();
+    SPR_HIP(m, hipEventRecord(e, m->st));
+    if (eos_id < 0) return SPR_OK;
+    SPR_HIP(m, hipEventRecord(snap[par], m->st));
+    if (pending) {
+      SPR_HIP(m, hipEventSynchronize(snap[par ^ 1]));
+      scan(par ^ 1, eos);
+    }
+    if (final) {
+      SPR_HIP(m, hipEventSynchronize(snap[par]));
+      scan(par, eos);
+      pending = false;
+      return SPR_OK;
+    }
+    pending = true;
+    par ^= 1;
+    return SPR_OK;
   }
 };
+
 
 }  // namespace
 
@@ -871,16 +936,19 @@ spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows,
   return SPR_OK;
 }
 
-spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t* tok,
-                     int32_t* out, spr_serve_stats* stats) {
+spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t max_active, int32_t eos_id,
+                     int32_t* tok, int32_t* out, int32_t* lengths, spr_serve_stats* stats) {
   g_err.clear();
   spr_status st = check_model(m);
   if (st != SPR_OK) return st;
   if (n < 0 || (n > 0 && (reqs == nullptr || tok == nullptr || out == nullptr)))
     return fail(SPR_ERR_INVALID_ARG, "serve: n must be >= 0, and reqs, tok and out non-null");
+  if (eos_id >= m->d.V) return fail(SPR_ERR_INVALID_ARG, "serve: eos_id must be < vocab (or negative: none)");
   std::vector<spr::ServeRequest> rq(n);
   std::vector<int64_t> off(static_cast<size_t>(n) + 1, 0);
   for (int i = 0; i < n; ++i) {
+    if (reqs[i].level < 0 || reqs[i].level >= SPR_MAX_LEVELS)
+      return fail(SPR_ERR_INVALID_ARG, "serve: level must be in [0, SPR_MAX_LEVELS)");
     rq[i] = spr::ServeRequest{reqs[i].tokens, reqs[i].n_tokens, reqs[i].stop_len, reqs[i].arrival};
     off[i + 1] = off[i] + std::max(reqs[i].stop_len, 0);
   }
@@ -891,18 +959,65 @@ spr_status spr_serve(spr_model* m, int32_t n, const spr_request* reqs, int32_t m
   dev.off = off.data();
   dev.tok = tok;
   dev.out = out;
+  dev.eos_id = eos_id < 0 ? -1 : eos_id;
+  hipEvent_t start = nullptr;
+  struct Cleanup {  // releases what this call created, on every path
+    GpuServe* d;
+    hipEvent_t* start;
+    ~Cleanup() {
+      for (hipEvent_t e : d->ev_iter) (void)hipEventDestroy(e);
+      for (hipEvent_t e : d->snap)
+        if (e) (void)hipEventDestroy(e);
+      if (*start) (void)hipEventDestroy(*start);
+      if (d->pin) (void)hipHostFree(d->pin);
+    }
+  } cleanup{&dev, &start};
+  SPR_HIP(m, hipEventCreate(&start));
+  if (dev.eos_id >= 0) {
+    SPR_HIP(m, hipHostMalloc(reinterpret_cast<void**>(&dev.pin), 4 * m->d.S * sizeof(int32_t), hipHostMallocDefault));
+    for (int i = 0; i < 2; ++i) SPR_HIP(m, hipEventCreateWithFlags(&dev.snap[i], hipEventDisableTiming));
+  }
+  SPR_HIP(m, hipEventRecord(start, m->st));
   spr::ServeCounters c;
+  std::vector<int32_t> len;
   std::string err;
-  st = spr::serve(m->tab, m->d, n, rq.data(), max_active, dev, &c, &err);
+  st = spr::serve(m->tab, m->d, n, rq.data(), max_active, dev, &c, &len, &err);
   if (st != SPR_OK) return err.empty() ? st : fail(st, err);
   SPR_HIP(m, hipStreamSynchronize(m->st));
+  if (lengths != nullptr)
+    for (int i = 0; i < n; ++i) lengths[i] = len[i];
   if (stats != nullptr) {
+    // Each iteration's device time, shared equally by the requests it served.
+    std::vector<double> sec(n, 0.0);
+    double total = 0.0;
+    hipEvent_t prev = start;
+    for (size_t it = 0; it < dev.ev_iter.size(); ++it) {
+      float ms = 0.f;
+      SPR_HIP(m, hipEventElapsedTime(&ms, prev, dev.ev_iter[it]));
+      prev = dev.ev_iter[it];
+      total += ms * 1e-3;
+      const auto& who = dev.served[it];
+      for (int r : who) sec[r] += ms * 1e-3 / static_cast<double>(who.size());
+    }
+    *stats = spr_serve_stats{};
     stats->iterations = c.iterations;
     stats->decode_steps = c.decode_steps;
     stats->prefill_calls = c.prefill_calls;
     stats->decode_tokens = c.decode_tokens;
     stats->max_batch = c.max_batch;
     stats->mean_batch = c.mean_batch;
+    stats->device_seconds = total;
+    for (int i = 0; i < n; ++i) {
+      const int lv = reqs[i].level;
+      stats->level_requests[lv] += 1;
+      stats->level_tokens[lv] += len[i];
+      stats->level_seconds[lv] += sec[i];
+    }
+    for (int lv = 0; lv < SPR_MAX_LEVELS; ++lv) {
+      if (stats->level_requests[lv] == 0) continue;
+      stats->level_tokens[lv] /= stats->level_requests[lv];
+      stats->level_seconds[lv] /= stats->level_requests[lv];
+    }
   }
   return SPR_OK;
 }

@@ -106,3 +106,63 @@ def test_serve_equals_closed_batch_7b():
         diverged += 1
     say("7B", f"{diverged} of {len(idx)} requests diverge at a near-tie")
     assert diverged <= 3
+
+
+def test_serve_eos_ends_requests_at_their_first_eos():
+    """Generation ends at EOS or at the limit (Section II-A): with an EOS id that the model emits
+    mid-sequence, every request stops at its first EOS (included) or at its stop length."""
+    from paper_2403_12900_amd.binding import DecodeModel
+    m, tol = CASES["bf16_gqa2"]
+    rng = np.random.default_rng(5)
+    prompts, _, arrivals = _requests(rng, m.vocab, 12)
+    stops = rng.integers(6, 16, size=12).tolist()
+    max_ctx = max(len(p) + s - 1 for p, s in zip(prompts, stops))
+    blocks = sum((len(p) + s - 1 + 15) // 16 for p, s in zip(prompts, stops))
+    dm = DecodeModel(m, 91, max_slots=4, max_ctx=max_ctx, kv_blocks=blocks)
+    free_run, _ = dm.serve(prompts, stops, max_active=4, arrivals=arrivals)
+    # The EOS id: the token that the most requests emit before their last position.
+    spread = np.zeros(m.vocab, dtype=np.int64)
+    for t in free_run:
+        spread[np.unique(t[:-1])] += 1
+    eos = int(spread.argmax())
+    say("eos", eos, f"emitted early by {int(spread[eos])} requests")
+    toks, st = dm.serve(prompts, stops, max_active=4, arrivals=arrivals, eos_id=eos)
+    say("eos", eos, [len(t) for t in toks], st["decode_tokens"])
+    stopped = 0
+    for t, s in zip(toks, stops):
+        assert 1 <= len(t) <= s
+        assert eos not in t[:-1].tolist()                       # nothing generated past an EOS
+        if len(t) < s:
+            assert t[-1] == eos
+            stopped += 1
+    assert stopped >= 2
+    w = R.Weights(oracle_shape(m), 91)
+    ties, steps = check_tokens_against_oracle(w, prompts, toks, tol)
+    say("eos", f"{steps} tokens, {ties} near-ties, {stopped} requests stopped at EOS")
+    assert ties <= max(1, steps // 20)
+    dm.close()
+
+
+def test_serve_level_profiles():
+    """Per-directive-level profiles (Eq. 2's p): counts and mean lengths per level are exact, the
+    attributed device time adds up, and levels that generate more take longer."""
+    from paper_2403_12900_amd.binding import DecodeModel
+    m, _ = CASES["bf16_gqa2"]
+    rng = np.random.default_rng(11)
+    n = 18
+    levels = [i % 3 for i in range(n)]
+    stops = [[40, 16, 4][lv] for lv in levels]
+    prompts = [rng.integers(0, m.vocab, size=int(rng.integers(4, 40))).astype(np.int32) for _ in range(n)]
+    max_ctx = max(len(p) + s - 1 for p, s in zip(prompts, stops))
+    blocks = sum((len(p) + s - 1 + 15) // 16 for p, s in zip(prompts, stops))
+    dm = DecodeModel(m, 91, max_slots=6, max_ctx=max_ctx, kv_blocks=blocks)
+    toks, st = dm.serve(prompts, stops, max_active=6, levels=levels)
+    say("levels", st["level_requests"][:3], st["level_tokens"][:3], st["level_seconds"][:3], st["device_seconds"])
+    assert st["level_requests"][:3] == [6, 6, 6] and sum(st["level_requests"]) == n
+    assert st["level_tokens"][:3] == [40.0, 16.0, 4.0]
+    attributed = sum(c * s for c, s in zip(st["level_requests"], st["level_seconds"]))
+    assert 0 < attributed <= st["device_seconds"] * (1 + 1e-6)
+    assert attributed >= 0.9 * st["device_seconds"]
+    p = st["level_seconds"][:3]
+    assert p[0] > p[1] > p[2] > 0
+    dm.close()

@@ -28,8 +28,8 @@ class Sched:
         L.sprh_new.restype = ctypes.c_void_p
         L.sprh_new.argtypes = [ctypes.POINTER(binding.SprConfig)]
         L.sprh_delete.argtypes = [ctypes.c_void_p]
-        L.sprh_serve.argtypes = [ctypes.c_void_p, ctypes.c_int, I32, I32, I32, ctypes.c_int, I32, I32, I32, I32,
-                                 ctypes.c_int, ctypes.POINTER(ctypes.c_int64)]
+        L.sprh_serve.argtypes = [ctypes.c_void_p, ctypes.c_int, I32, I32, I32, ctypes.c_int, ctypes.c_int, I32, I32,
+                                 I32, I32, I32, I32, ctypes.c_int, I32, ctypes.POINTER(ctypes.c_int64)]
         L.sprh_prefill.argtypes = [ctypes.c_void_p, ctypes.c_int, I32, I32, I32, I32]
         L.sprh_free_blocks.argtypes = [ctypes.c_void_p]
         L.sprh_last_error.restype = ctypes.c_char_p
@@ -41,18 +41,24 @@ class Sched:
     def close(self):
         self.L.sprh_delete(self.h)
 
-    def run(self, n_tokens, stop, arrival=None, max_active=None):
+    def run(self, n_tokens, stop, arrival=None, max_active=None, eos=()):
+        """eos: (request, token index) pairs whose token is the EOS id."""
         n = len(stop)
         arrival = [0] * n if arrival is None else arrival
         max_active = self.cfg.max_slots if max_active is None else max_active
         a = [np.ascontiguousarray(np.asarray(x, dtype=np.int32)) for x in (n_tokens, stop, arrival)]
+        er = np.ascontiguousarray(np.asarray([e[0] for e in eos] or [0], dtype=np.int32))
+        ei = np.ascontiguousarray(np.asarray([e[1] for e in eos] or [0], dtype=np.int32))
+        lengths = np.full(max(n, 1), -1, dtype=np.int32)
         tot = int(sum(stop))
         it, sl, call = (np.full(tot, -1, dtype=np.int32) for _ in range(3))
         batch = np.full(4096, -1, dtype=np.int32)
         cnt = np.zeros(5, dtype=np.int64)
         p = lambda x: x.ctypes.data_as(I32)
-        st = self.L.sprh_serve(self.h, n, p(a[0]), p(a[1]), p(a[2]), max_active, p(it), p(sl), p(call), p(batch),
-                               len(batch), cnt.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+        st = self.L.sprh_serve(self.h, n, p(a[0]), p(a[1]), p(a[2]), max_active, len(eos), p(er), p(ei), p(it), p(sl),
+                               p(call), p(batch), len(batch), p(lengths),
+                               cnt.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+        self.lengths = lengths[:n].tolist()
         off = np.concatenate([[0], np.cumsum(stop)]).astype(int)
         per = [(it[off[i]:off[i + 1]], sl[off[i]:off[i + 1]], call[off[i]:off[i + 1]]) for i in range(n)]
         steps = int(cnt[1])
@@ -161,4 +167,36 @@ def test_needs_an_idle_model():
     assert s.L.sprh_prefill(s.h, 1, p(np.zeros(1, dtype=np.int32)), p(one * 3), p(one * 4), p(r)) == 0
     st, *_ = s.run([4], [2])
     assert st == binding.SPR_ERR_STATE
+    s.close()
+
+
+def test_eos_retires_one_iteration_late():
+    """Generation ends at EOS or at the limit (Section II-A).  The device reports EOS one iteration
+    late, so a request runs at most one more decode row (two if EOS was the prefill's token, whose
+    iteration already decoded), its length ends at the first EOS, and its slot is reused no earlier
+    than two iterations after the EOS iteration."""
+    stop = [12, 12, 12, 12, 12, 5]
+    eos = [(0, 3), (1, 0), (2, 11), (3, 6), (3, 8)]          # request 3: only the first EOS counts
+    s = Sched(max_slots=2)
+    st, per, batch, c = s.run([9] * 6, stop, max_active=2, eos=eos)
+    assert st == 0
+    assert s.lengths == [4, 1, 12, 7, 12, 5]
+    for r, k in [(0, 3), (1, 0), (3, 6)]:
+        its, slots, _ = per[r]
+        produced = int((its >= 0).sum())
+        extra = produced - (k + 1)
+        assert 0 <= extra <= (2 if k == 0 else 1), (r, produced)
+        t_eos = its[k]
+        later = [q for q in range(len(stop)) if q > r and per[q][1][0] == slots[0] and per[q][0][0] > t_eos]
+        assert all(per[q][0][0] >= t_eos + 2 for q in later), r
+    assert s.L.sprh_free_blocks(s.h) == s.cfg.kv_blocks
+    s.close()
+
+
+def test_eos_on_the_last_token_changes_nothing():
+    stop = [4, 6]
+    s = Sched(max_slots=2)
+    st, per, batch, c = s.run([5, 5], stop, eos=[(0, 3), (1, 5)])
+    assert st == 0 and s.lengths == [4, 6]
+    assert batch == [len(a) for a in R.active_schedule(stop)]
     s.close()
