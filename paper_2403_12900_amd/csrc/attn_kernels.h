@@ -14,9 +14,10 @@
 //              re-used in place as the B operand: no shuffle, no LDS
 // The four waves are merged through LDS (log-sum-exp), each wave combining a
 // quarter of the head dimensions.  A row whose context needs one split writes
-// its output directly; otherwise each split writes a partial (max, sum,
-// unnormalised output) and k_attn_merge combines them.  The grid holds only
-// (row, split) pairs with work.
+// its output directly; otherwise each split publishes a partial (max, sum,
+// unnormalised output) and counts itself in, and the split that arrives last
+// merges them all (one launch; no work-group ever waits on another).  The
+// grid holds only (row, split) pairs with work.
 // bf16 keys are multiplied by q split into hi + lo bf16 parts, so the scores
 // carry fp32-level precision of q.
 #pragma once
@@ -32,11 +33,27 @@ struct AttnArgs {
   const int32_t* bt;      // [slots][mb]
   void* act;              // output, K-block-major over H * hd
   float* part;            // [flat split][H][hd + 4]: m, l, -, -, o[hd]
+  int32_t* cnt;           // [rows][Hkv] arrived splits; zero between launches
   int n_rows, H, Hkv, G, mb, bpw, Rp;
   float qscale;           // log2(e) / sqrt(hd)
   RowSlotPos rows;
   int split_start[kRows + 1];  // first flat split index of each row; [n_rows] = total
 };
+
+// Agent-coherent 8-byte store and load (relaxed device-scope atomics): a
+// work-group on any XCD reads the stored value once the storing wave's vmcnt
+// has drained, without a write-back of the storing XCD's L2.
+__device__ __forceinline__ void store_coherent2(float* p, float x, float y) {
+  const uint64_t v = static_cast<uint64_t>(__float_as_uint(x)) | (static_cast<uint64_t>(__float_as_uint(y)) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_coherent2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
+}
+
+template <class AP, int HD>
+__device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns);
 
 // K and V of one 16-position block of one KV head, in registers: NF K
 // operands and NV 16-byte V loads (two bf16 V^T operands or one fp32 operand
@@ -275,41 +292,50 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
       for (int r = 0; r < 4; ++r) R[k][r] += cw[w] * o[r];
     }
   }
-  if (!hv) return;
   const int hq = kvh * a.G + h;
   if (nsplit == 1) {
+    if (!hv) return;
     const float inv = 1.f / L;
     typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
     for (int k = 0; k < EPW; ++k)
       store_act4<AP>(act, a.Rp, b, hq * HD + 16 * (wave * EPW + k) + 4 * g, R[k][0] * inv, R[k][1] * inv,
                      R[k][2] * inv, R[k][3] * inv);
-  } else {
-    float* pp = a.part + (static_cast<size_t>(f) * a.H + hq) * (HD + 4);
-    if (wave == 0 && g == 0) {
-      pp[0] = M;
-      pp[1] = L;
-    }
-#pragma unroll
-    for (int k = 0; k < EPW; ++k)
-      *reinterpret_cast<float4*>(pp + 4 + 16 * (wave * EPW + k) + 4 * g) = make_float4(R[k][0], R[k][1], R[k][2], R[k][3]);
+    return;
   }
+  // Several splits: publish this split's partial, then count it in.  Each
+  // partial is written with agent-coherent stores and completed (vmcnt 0)
+  // before the work-group's arrival is counted, so whichever split arrives
+  // last reads every partial with agent-coherent loads: no cache write-back
+  // and no wait on another work-group.
+  if (hv) {
+    float* pp = a.part + (static_cast<size_t>(f) * a.H + hq) * (HD + 4);
+    if (wave == 0 && g == 0) store_coherent2(pp, M, L);
+#pragma unroll
+    for (int k = 0; k < EPW; ++k) {
+      float* o = pp + 4 + 16 * (wave * EPW + k) + 4 * g;
+      store_coherent2(o, R[k][0], R[k][1]);
+      store_coherent2(o + 2, R[k][2], R[k][3]);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's partial stores are complete
+  __shared__ int last;
+  __syncthreads();
+  int32_t* cnt = a.cnt + b * a.Hkv + kvh;
+  if (threadIdx.x == 0) last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1;
+  __syncthreads();
+  if (!last) return;
+  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  merge_splits<AP, HD>(a, b, kvh, a.split_start[b], nsplit);
 }
 
-// Log-sum-exp merge of the KV splits of one (row, KV head), for rows whose
-// context needed more than one split.  Splits are taken kChunk at a time, all
-// of a chunk's loads issued before any is combined (indexes past the last
-// split re-read it and are then ignored).  (A last-arriving split could merge
-// instead of a second launch, but the device-scope release that needs -- a
-// write-back of the XCD's L2 by every split -- measured ten times slower on
-// MI355X.)
+// Log-sum-exp merge of the nsplit partials of one (row, KV head), run by the
+// split that arrived last.  Splits are taken kChunk at a time, all of a
+// chunk's loads issued before any is combined (indexes past the last split
+// re-read it and are then ignored).
 template <class AP, int HD>
-__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
-  constexpr int kChunk = 32;
-  const int b = blockIdx.x, kvh = blockIdx.y;
-  const int f0 = a.split_start[b];
-  const int ns = a.split_start[b + 1] - f0;
-  if (ns <= 1) return;
+__device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns) {
+  constexpr int kChunk = 16;
   typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
   const size_t stride = static_cast<size_t>(a.H) * (HD + 4);
   for (int idx = threadIdx.x; idx < a.G * HD; idx += 256) {
@@ -321,9 +347,10 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
 #pragma unroll
       for (int k = 0; k < kChunk; ++k) {
         const float* pt = pp + static_cast<size_t>(min(t0 + k, ns - 1)) * stride;
-        m[k] = pt[0];
-        l[k] = pt[1];
-        o[k] = pt[4 + dd];
+        const float2 ml = load_coherent2(pt);
+        m[k] = ml.x;
+        l[k] = ml.y;
+        o[k] = __hip_atomic_load(pt + 4 + dd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       float Mn = M;
 #pragma unroll

@@ -110,6 +110,8 @@ Layout layout(const Dims& d) {
   l.off_act1 = take(l.act_bytes);
   l.off_q = take(static_cast<size_t>(kPrefillRows) * d.H * d.hd * sizeof(float));
   l.off_part = take(static_cast<size_t>(kMaxSplits) * d.H * (d.hd + 4) * sizeof(float));
+  // Split arrival counters of decode attention, one per (row, KV head); zero between launches.
+  l.off_cnt = take(static_cast<size_t>(kMaxRows) * d.Hkv * sizeof(int32_t));
   l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
   l.off_prow = take(static_cast<size_t>(kPrefillRows) * 4 * sizeof(int32_t));
   l.off_ptile = take(static_cast<size_t>(kPrefillTiles) * 4 * sizeof(int32_t));

@@ -36,7 +36,7 @@ struct Layout {
   size_t wqkv, wo, w13, w2;        // per-layer strides of the tiled weights (bytes)
   size_t off_wqkv, off_wo, off_w13, off_w2, off_wlm, off_emb;
   size_t off_rope, off_kc, off_vc, kv_layer_stride, off_bt;
-  size_t off_x, off_act0, off_act1, act_bytes, off_q, off_part, off_amax;
+  size_t off_x, off_act0, off_act1, act_bytes, off_q, off_part, off_cnt, off_amax;
   size_t off_prow, off_ptile, off_rs;  // prefill chunk: row table, query tiles, RMSNorm scales
   size_t total;
 };

@@ -135,6 +135,7 @@ struct Ptrs {
   char* act(int i) const { return ws + (i == 0 ? l->off_act0 : l->off_act1); }
   float* q() const { return reinterpret_cast<float*>(ws + l->off_q); }
   float* part() const { return reinterpret_cast<float*>(ws + l->off_part); }
+  int32_t* cnt() const { return reinterpret_cast<int32_t*>(ws + l->off_cnt); }
   float2* amax() const { return reinterpret_cast<float2*>(ws + l->off_amax); }
   float2* rope() const { return reinterpret_cast<float2*>(ws + l->off_rope); }
   PrefillRow* prow() const { return reinterpret_cast<PrefillRow*>(ws + l->off_prow); }
@@ -225,10 +226,6 @@ template <class P, class KP, int HD>
 spr_status launch_attention(spr_model* m, const AttnArgs& a) {
   k_attn_decode<KP, P, HD><<<dim3(a.split_start[a.n_rows], a.Hkv), 256, 0, m->st>>>(a);
   SPR_LAUNCHED(m, "k_attn_decode");
-  if (a.split_start[a.n_rows] > a.n_rows) {  // some row has more than one split
-    k_attn_merge<P, HD><<<dim3(a.n_rows, a.Hkv), 256, 0, m->st>>>(a);
-    SPR_LAUNCHED(m, "k_attn_merge");
-  }
   return SPR_OK;
 }
 
@@ -306,6 +303,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       a.bt = p.bt();
       a.act = p.act(1);
       a.part = p.part();
+      a.cnt = p.cnt();
       a.n_rows = n;
       a.H = d.H;
       a.Hkv = d.Hkv;
@@ -760,6 +758,7 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
   hipError_t e = hipMemcpyAsync(p.rope(), rope.data(), rope.size() * sizeof(float), hipMemcpyHostToDevice, m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.bt(), 0, static_cast<size_t>(d.S) * d.mb * sizeof(int32_t), m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(0), 0, lay.act_bytes, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.cnt(), 0, static_cast<size_t>(spr::kMaxRows) * d.Hkv * sizeof(int32_t), m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(1), 0, lay.act_bytes, m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kPrefillRows) * d.d * sizeof(float), m->st);
   if (e == hipSuccess) e = hipStreamSynchronize(m->st);
