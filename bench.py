@@ -177,6 +177,25 @@ def time_prefill(model, m, wl, stops, reps: int = 3):
             "peak_tflops": PEAK_BF16_TFLOPS, "mfma_frac": round(tflops * issue / PEAK_BF16_TFLOPS, 4)}
 
 
+def gpu_energy_reader():
+    """A function returning GPU 0's accumulated energy in joules (amd-smi energy counter), or None
+    when amd-smi cannot read it here."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+        handle = amdsmi.amdsmi_get_processor_handles()[0]
+
+        def read():
+            c = amdsmi.amdsmi_get_energy_count(handle)
+            return c["energy_accumulator"] * c["counter_resolution"] * 1e-6
+
+        read()
+        return read
+    except Exception as exc:  # no amd-smi, no permission, or no counter on this device
+        log(f"energy counter unavailable: {exc}")
+        return None
+
+
 def time_serving(cfg, n_req: int = 96, max_active: int = 32):
     """Continuous batching (spr_serve) against closed batches, on the same
     requests: n_req requests drawn with the workload's recipe, all waiting at
@@ -200,8 +219,11 @@ def time_serving(cfg, n_req: int = 96, max_active: int = 32):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     n_lv = len(cfg.workload.prefix_lens)
+    energy = gpu_energy_reader()
+    j0 = energy() if energy else None
     _, st = model.serve(prompts, stops, max_active, levels=[int(x) for x in wl.levels])
     cont = time.perf_counter() - t0
+    joules = energy() - j0 if energy else None
     tok = model.new_token_buffer()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -230,7 +252,12 @@ def time_serving(cfg, n_req: int = 96, max_active: int = 32):
             # iteration's time shared equally by the requests it served.
             "level_requests": st["level_requests"][:n_lv],
             "level_mean_tokens": [round(x, 1) for x in st["level_tokens"][:n_lv]],
-            "level_seconds_per_request": [round(x, 4) for x in st["level_seconds"][:n_lv]]}
+            "level_seconds_per_request": [round(x, 4) for x in st["level_seconds"][:n_lv]],
+            # Eq. 2's per-level e: the amd-smi energy of the whole serving run, attributed to each
+            # request in proportion to its share of device time (the same sharing as p).
+            "energy_joules": None if joules is None else round(joules, 2),
+            "level_joules_per_request": None if joules is None or st["device_seconds"] <= 0 else
+            [round(joules * x / st["device_seconds"], 3) for x in st["level_seconds"][:n_lv]]}
 
 
 def cpu_baseline(cfg, wl, seconds: float):
@@ -364,6 +391,8 @@ def main():
                      ("lm_head", m.vocab * m.d_model)):
         u = model.time_projection(name, n_probe, 50)
         others[name] = {"us": round(u, 2), "gbps": round(el * 2 / (u * 1e-6) / 1e9, 1)}
+    ceiling, ceiling_bytes = model.read_ceiling(5)
+    log(f"read ceiling: {ceiling:.0f} GB/s over {ceiling_bytes / 1e9:.2f} GB of weights")
     traffic = measured_traffic(per_launch)
     log(f"gate/up kernel: {us:.2f} us per launch, {achieved:.0f} GB/s; others {others}")
 
@@ -382,6 +411,10 @@ def main():
         "data": "synthetic",
         "achieved_hbm_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+        # The measured read ceiling: every weight matrix streamed with the projections' load form
+        # (16-byte nontemporal loads, 8 in flight per thread) and no arithmetic.
+        "read_ceiling_gbps": round(ceiling, 1),
+        "frac_of_read_ceiling": round(gbps / ceiling, 4),
         "config": {"workload": cfg.name, "batch": B, "decode_steps": st["steps"],
                    "decode_tokens_per_step": tokens, "avg_active": round(st["avg_active"], 3),
                    "algorithmic_bytes_per_step": st["bytes"], "parallelism": "none (1 GPU)"},

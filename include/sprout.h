@@ -178,6 +178,18 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
  */
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
 
+/*
+ * Measurement aid: the HBM read ceiling of the projections' load form.
+ * Streams every weight matrix a decode step reads (all layers' projections
+ * and the LM head, resident in the model's workspace) once per rep with
+ * 16-byte nontemporal loads, 8 in flight per thread and no arithmetic, brackets
+ * the reps with HIP events on the model's stream, waits, and writes the mean
+ * read rate in GB/s (1e9 bytes/s) to *gbps and the bytes read per rep to
+ * *bytes.  Reads only; model state is untouched.  reps 1..1000; null outputs
+ * are SPR_ERR_INVALID_ARG.  Synchronous.
+ */
+spr_status spr_time_read_ceiling(spr_model* m, int32_t reps, double* gbps, uint64_t* bytes);
+
 #define SPR_MAX_LEVELS 8 /* directive levels a serving run can profile */
 
 /* One request of a serving run (host memory, read during the call). */

@@ -86,6 +86,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_time_projection.restype = ctypes.c_int
     L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_float)]
+    L.spr_time_read_ceiling.restype = ctypes.c_int
+    L.spr_time_read_ceiling.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_uint64)]
     L.spr_serve.restype = ctypes.c_int
     L.spr_serve.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(SprRequest), ctypes.c_int32, ctypes.c_int32, vp, vp,
                             _I32P, ctypes.POINTER(SprServeStats)]
@@ -200,6 +203,12 @@ class DecodeModel:
         out = ctypes.c_float()
         _check(self.lib.spr_time_projection(self.h, self.PROJECTIONS[projection], n_rows, reps, ctypes.byref(out)))
         return float(out.value)
+
+    def read_ceiling(self, reps: int = 5):
+        """(GB/s, bytes per pass): plain streaming read of every weight matrix, timed on the model's stream."""
+        gbps, nbytes = ctypes.c_double(), ctypes.c_uint64()
+        _check(self.lib.spr_time_read_ceiling(self.h, reps, ctypes.byref(gbps), ctypes.byref(nbytes)))
+        return float(gbps.value), int(nbytes.value)
 
     def serve(self, prompts: Sequence[Sequence[int]], stop_lens: Sequence[int], max_active: int,
               arrivals: Optional[Sequence[int]] = None, levels: Optional[Sequence[int]] = None, eos_id: int = -1):

@@ -900,6 +900,44 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
   return SPR_OK;
 }
 
+spr_status spr_time_read_ceiling(spr_model* m, int32_t reps, double* gbps, uint64_t* bytes) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (gbps == nullptr || bytes == nullptr) return fail(SPR_ERR_INVALID_ARG, "time_read_ceiling: null output");
+  if (reps < 1 || reps > 1000) return fail(SPR_ERR_INVALID_ARG, "time_read_ceiling: reps in [1, 1000]");
+  // Every weight matrix a decode step streams: all layers' projections and the LM head.
+  const size_t nbytes = m->lay.off_emb - m->lay.off_wqkv;
+  const uint4* base = reinterpret_cast<const uint4*>(m->ws + m->lay.off_wqkv);
+  int dev = 0, ncu = 0;
+  SPR_HIP(m, hipGetDevice(&dev));
+  SPR_HIP(m, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
+  hipEvent_t e0, e1;
+  SPR_HIP(m, hipEventCreate(&e0));
+  hipError_t e = hipEventCreate(&e1);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return hip_fail(m, "hipEventCreate", e);
+  }
+  Ptrs p{m->ws, &m->lay};
+  uint32_t* sink = reinterpret_cast<uint32_t*>(p.amax());
+  e = hipEventRecord(e0, m->st);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) {
+    k_read_stream<<<ncu * 8, 256, 0, m->st>>>(base, nbytes / 16, sink);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipEventRecord(e1, m->st);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return hip_fail(m, "time_read_ceiling", e);
+  *bytes = static_cast<uint64_t>(nbytes);
+  *gbps = static_cast<double>(nbytes) * reps / (static_cast<double>(ms) * 1e-3) / 1e9;
+  return SPR_OK;
+}
+
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us) {
   g_err.clear();
   spr_status st = check_model(m);

@@ -73,4 +73,31 @@ __global__ __launch_bounds__(256) void k_argmax_final(ArgmaxArgs a) {
   }
 }
 
+// Streaming read of n16 16-byte words with the projections' load form
+// (nontemporal 16-byte loads, kReadUnroll in flight per thread): the read
+// rate this memory path reaches with no arithmetic attached.  Full chunks of
+// 256 * kReadUnroll words run unpredicated; the tail is read word by word.
+// The XOR of every word read goes to sink only when it equals a fixed
+// constant, so no load can be dropped and the store practically never runs.
+constexpr int kReadUnroll = 8;
+__global__ __launch_bounds__(256) void k_read_stream(const uint4* __restrict__ p, size_t n16, uint32_t* sink) {
+  constexpr size_t kChunk = 256 * kReadUnroll;
+  const size_t full = n16 / kChunk;
+  uint32_t acc = 0;
+  for (size_t c = blockIdx.x; c < full; c += gridDim.x) {
+    const uint4* q = p + c * kChunk + threadIdx.x;
+    uint4 v[kReadUnroll];
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) v[u] = load_weight<true>(q + u * 256);
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  if (blockIdx.x == 0)
+    for (size_t k = full * kChunk + threadIdx.x; k < n16; k += 256) {
+      const uint4 v = p[k];
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+  if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
 }  // namespace sprk

@@ -162,6 +162,23 @@ def test_forced_tokens_and_in_place_buffer():
     dm.close()
 
 
+def test_read_ceiling_streams_every_weight_matrix():
+    """The read-ceiling probe reads every projection and the LM head once per pass, and checks its arguments."""
+    m, _, _ = TOY_CASES["bf16_mha_hd64_ragged"]
+    from paper_2403_12900_amd.binding import DecodeModel, SproutError
+    dm = DecodeModel(m, 78, max_slots=2, max_ctx=64)
+    gbps, nbytes = dm.read_ceiling(3)
+    e = 2 if m.bf16 else 4
+    raw = e * (m.n_layers * ((m.n_heads + 2 * m.n_kv_heads) * m.head_dim * m.d_model
+                             + m.d_model * m.n_heads * m.head_dim + 3 * m.d_ff * m.d_model) + m.vocab * m.d_model)
+    say("read ceiling", gbps, nbytes, raw)
+    assert raw <= nbytes <= 1.25 * raw + 4096 * (4 * m.n_layers + 1)   # tile padding and 256-byte alignment only
+    assert gbps > 0
+    with pytest.raises(SproutError):
+        dm.read_ceiling(0)
+    dm.close()
+
+
 def test_rewind_regenerates_identically():
     m, _, _ = TOY_CASES["bf16_gqa4_hd128_wide_o"]
     say("rewind")
