@@ -179,6 +179,24 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
 
 /*
+ * How a decode pass (spr_decode_step, and the decode steps of spr_serve) runs
+ * the layer stack (Section II-A's per-token forward pass; the choice changes
+ * launches, not results beyond floating-point summation order):
+ *   0  one launch per kernel: QKV projection, attention, O, gate/up, down
+ *      (the default);
+ *   1  one persistent launch per layer for passes of at most 32 rows: the
+ *      five phases run on a grid of resident work-groups (CUs x up to 3)
+ *      separated by grid barriers; larger passes use mode 0.  If a grid
+ *      barrier does not complete (a work-group that is never scheduled), the
+ *      launch still ends and the next call on the model fails with
+ *      SPR_ERR_HIP.
+ * SPR_ERR_INVALID_ARG for another mode, or for 1 when the persistent launch
+ * cannot keep its grid resident on this device.  Takes effect from the next
+ * pass.
+ */
+spr_status spr_set_decode_mode(spr_model* m, int32_t mode);
+
+/*
  * Measurement aid: the HBM read ceiling of the projections' load form.
  * Streams every weight matrix a decode step reads (all layers' projections
  * and the LM head, resident in the model's workspace) once per rep with

@@ -86,6 +86,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_time_projection.restype = ctypes.c_int
     L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_float)]
+    L.spr_set_decode_mode.restype = ctypes.c_int
+    L.spr_set_decode_mode.argtypes = [vp, ctypes.c_int32]
     L.spr_time_read_ceiling.restype = ctypes.c_int
     L.spr_time_read_ceiling.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_uint64)]
@@ -203,6 +205,10 @@ class DecodeModel:
         out = ctypes.c_float()
         _check(self.lib.spr_time_projection(self.h, self.PROJECTIONS[projection], n_rows, reps, ctypes.byref(out)))
         return float(out.value)
+
+    def set_decode_mode(self, mode: int):
+        """0: one launch per kernel; 1: one persistent launch per layer for passes of at most 32 rows."""
+        _check(self.lib.spr_set_decode_mode(self.h, mode))
 
     def read_ceiling(self, reps: int = 5):
         """(GB/s, bytes per pass): plain streaming read of every weight matrix, timed on the model's stream."""

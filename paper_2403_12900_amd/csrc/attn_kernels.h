@@ -52,7 +52,7 @@ __device__ __forceinline__ float2 load_coherent2(const float* p) {
   return make_float2(__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
 }
 
-template <class AP, int HD>
+template <class AP, int HD, bool kCoh>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns);
 
 // K and V of one 16-position block of one KV head, in registers: NF K
@@ -145,15 +145,26 @@ struct KVBlock {
 // block ids of its run come in one vector load up front, so each block costs
 // one memory round trip.  Branch conditions are wave-uniform; the partial
 // last block of the context is masked by selects.
-template <class P, class AP, int HD>
-__global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
+// LDS of one attention work item: the four waves' outputs and (max, sum).
+template <int HD>
+struct AttnSmem {
+  f32x4_t so[4][HD / 16][64];
+  float2 sml[4][64];
+  int last;
+};
+
+// The body of k_attn_decode for work item (flat split f, KV head kvh), run by
+// all four waves of the calling work-group.  kCoh: the output activation is
+// read by other work-groups of the same launch (the persistent layer kernel),
+// so it goes out as agent-coherent stores.
+template <class P, class AP, int HD, bool kCoh>
+__device__ __forceinline__ void attn_decode_unit(const AttnArgs& a, int f, int kvh, AttnSmem<HD>* sm) {
   using E = typename P::elem;
   using Blk = KVBlock<P, HD>;
   constexpr bool kBf16 = sizeof(E) == 2;
   constexpr int NF = Blk::NF;
   constexpr int NE = HD / 16;     // output operands (16 dims each)
   constexpr int EPW = NE / 4;     // output operands each wave merges and stores
-  const int f = blockIdx.x, kvh = blockIdx.y;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // Row of this work-group = number of rows whose splits all precede f (the
@@ -262,17 +273,15 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   // operands [w * EPW, (w + 1) * EPW).  Wave 0 always holds at least one
   // block (its run starts the split), so M is finite; waves without blocks
   // carry m = -inf and weigh 0.
-  __shared__ f32x4_t so[4][NE][64];
-  __shared__ float2 sml[4][64];
-  sml[wave][lane] = make_float2(m_run, l_run);
+  sm->sml[wave][lane] = make_float2(m_run, l_run);
 #pragma unroll
-  for (int e = 0; e < NE; ++e) so[wave][e][lane] = O[e];
+  for (int e = 0; e < NE; ++e) sm->so[wave][e][lane] = O[e];
   __syncthreads();
   float2 ml[4];
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    ml[w] = sml[w][lane];
+    ml[w] = sm->sml[w][lane];
     M = fmaxf(M, ml[w].x);
   }
   float cw[4], L = 0.f;
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
     R[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const f32x4_t o = so[w][wave * EPW + k][lane];
+      const f32x4_t o = sm->so[w][wave * EPW + k][lane];
 #pragma unroll
       for (int r = 0; r < 4; ++r) R[k][r] += cw[w] * o[r];
     }
@@ -298,9 +307,11 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
     const float inv = 1.f / L;
     typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
 #pragma unroll
-    for (int k = 0; k < EPW; ++k)
-      store_act4<AP>(act, a.Rp, b, hq * HD + 16 * (wave * EPW + k) + 4 * g, R[k][0] * inv, R[k][1] * inv,
-                     R[k][2] * inv, R[k][3] * inv);
+    for (int k = 0; k < EPW; ++k) {
+      const int n0 = hq * HD + 16 * (wave * EPW + k) + 4 * g;
+      if constexpr (kCoh) act_store4_coh<AP>(act, a.Rp, b, n0, R[k][0] * inv, R[k][1] * inv, R[k][2] * inv, R[k][3] * inv);
+      else store_act4<AP>(act, a.Rp, b, n0, R[k][0] * inv, R[k][1] * inv, R[k][2] * inv, R[k][3] * inv);
+    }
     return;
   }
   // Several splits: publish this split's partial, then count it in.  Each
@@ -319,21 +330,27 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
     }
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's partial stores are complete
-  __shared__ int last;
   __syncthreads();
   int32_t* cnt = a.cnt + b * a.Hkv + kvh;
-  if (threadIdx.x == 0) last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1;
+  if (threadIdx.x == 0)
+    sm->last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1;
   __syncthreads();
-  if (!last) return;
+  if (!sm->last) return;
   if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  merge_splits<AP, HD>(a, b, kvh, a.split_start[b], nsplit);
+  merge_splits<AP, HD, kCoh>(a, b, kvh, a.split_start[b], nsplit);
+}
+
+template <class P, class AP, int HD>
+__global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
+  __shared__ AttnSmem<HD> sm;
+  attn_decode_unit<P, AP, HD, false>(a, blockIdx.x, blockIdx.y, &sm);
 }
 
 // Log-sum-exp merge of the nsplit partials of one (row, KV head), run by the
 // split that arrived last.  Splits are taken kChunk at a time, all of a
 // chunk's loads issued before any is combined (indexes past the last split
 // re-read it and are then ignored).
-template <class AP, int HD>
+template <class AP, int HD, bool kCoh>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns) {
   constexpr int kChunk = 16;
   typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
@@ -366,7 +383,8 @@ __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, 
       }
       M = Mn;
     }
-    act_store<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
+    if constexpr (kCoh) act_store_coh<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
+    else act_store<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
   }
 }
 

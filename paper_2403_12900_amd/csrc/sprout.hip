@@ -27,6 +27,7 @@
 #include <vector>
 
 #include "attn_kernels.h"
+#include "layer_kernels.h"
 #include "gemm_kernels.h"
 #include "host_state.h"
 #include "prefill_kernels.h"
@@ -37,6 +38,9 @@ using namespace sprk;
 
 static_assert(spr::kPrefillRows == sprk::kPrefillRows, "prefill chunk size");
 static_assert(spr::kMaxRows == sprk::kRows, "decode pass size");
+static_assert(spr::kBarBytes == 4 * sprk::kBarWords, "grid barrier words");
+static_assert(sizeof(sprk::LayerArgs) + sizeof(sprk::LayerEpis<sprk::BF16, sprk::F32>) <= 4096,
+              "persistent layer launch arguments exceed the kernel argument segment");
 
 struct spr_model {
   spr::Dims d{};
@@ -47,6 +51,17 @@ struct spr_model {
   std::vector<int32_t> bt_row;
   bool sticky = false;
   uint64_t seed = 0;
+  // Persistent layer launch (decode mode 1): grid size (0 = unavailable), the
+  // barrier generation the next launch starts from, and the timeout flag in
+  // mapped pinned host memory (host and device views).
+  int decode_mode = 0;
+  int layer_grid = 0;
+  unsigned bar_gen = 0;
+  int* err_host = nullptr;
+  int* err_dev = nullptr;
+  ~spr_model() {
+    if (err_host != nullptr) (void)hipHostFree(err_host);
+  }
 };
 
 namespace {
@@ -132,7 +147,10 @@ struct Ptrs {
   char* vc(int layer) const { return ws + l->off_vc + l->kv_layer_stride * layer; }
   int32_t* bt() const { return reinterpret_cast<int32_t*>(ws + l->off_bt); }
   float* x() const { return reinterpret_cast<float*>(ws + l->off_x); }
-  char* act(int i) const { return ws + (i == 0 ? l->off_act0 : l->off_act1); }
+  char* act(int i) const {
+    return ws + (i == 0 ? l->off_act0 : i == 1 ? l->off_act1 : i == 2 ? l->off_act2 : l->off_act3);
+  }
+  unsigned* bar() const { return reinterpret_cast<unsigned*>(ws + l->off_bar); }
   float* q() const { return reinterpret_cast<float*>(ws + l->off_q); }
   float* part() const { return reinterpret_cast<float*>(ws + l->off_part); }
   int32_t* cnt() const { return reinterpret_cast<int32_t*>(ws + l->off_cnt); }
@@ -229,6 +247,130 @@ spr_status launch_attention(spr_model* m, const AttnArgs& a) {
   return SPR_OK;
 }
 
+// Whether the persistent layer launch streams gate/up in one-wave two-tile
+// units (the per-kernel path's shape for projections this wide).
+inline bool wide_gate_up(const spr::Dims& d) { return d.nt_13 >= 1024 && d.nt_13 % 2 == 0; }
+
+// Attention arguments of one layer over rs (kv splits of bpw blocks per wave).
+template <class P, class KP>
+AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int Rp, int bpw, void* act) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  AttnArgs a{};
+  a.q = p.q();
+  a.kc = p.kc(l);
+  a.vc = p.vc(l);
+  a.bt = p.bt();
+  a.act = act;
+  a.part = p.part();
+  a.cnt = p.cnt();
+  a.n_rows = rs.n;
+  a.H = d.H;
+  a.Hkv = d.Hkv;
+  a.G = d.G;
+  a.mb = d.mb;
+  a.bpw = bpw;
+  a.Rp = Rp;
+  a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
+  a.rows = sp;
+  a.split_start[0] = 0;
+  for (int r = 0; r < rs.n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw);
+  return a;
+}
+
+// One layer of a decode pass of at most 32 rows as a single persistent launch
+// (k_decode_layer): the phases read act(0), act(1), act(2), act(3) and the
+// down projection writes act(0) for the next layer.
+template <class P, class KP>
+spr_status launch_layer(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int JT, int bpw) {
+  const spr::Dims& d = m->d;
+  Ptrs p{m->ws, &m->lay};
+  using E = typename P::elem;
+  const int n = rs.n, Rp = 16 * JT;
+  if (m->bar_gen > (1u << 24)) {  // keep the accumulated counts far from overflow
+    SPR_HIP(m, hipMemsetAsync(p.bar(), 0, spr::kBarBytes, m->st));
+    m->bar_gen = 0;
+  }
+  LayerArgs a{};
+  a.wqkv = reinterpret_cast<const uint4*>(p.wqkv(l));
+  a.wo = reinterpret_cast<const uint4*>(p.wo(l));
+  a.w13 = reinterpret_cast<const uint4*>(p.w13(l));
+  a.w2 = reinterpret_cast<const uint4*>(p.w2(l));
+  a.act_in = reinterpret_cast<const uint4*>(p.act(0));
+  a.act_attn = reinterpret_cast<const uint4*>(p.act(1));
+  a.act_mid = reinterpret_cast<const uint4*>(p.act(2));
+  a.act_h = reinterpret_cast<const uint4*>(p.act(3));
+  a.n_rows = n;
+  a.Rp = Rp;
+  a.nt_qkv = d.nt_qkv;
+  a.nt_o = d.nt_o;
+  a.nt_13 = d.nt_13;
+  a.nt_2 = d.nt_2;
+  a.kb_d = d.kb_d;
+  a.kb_o = d.kb_o;
+  a.kb_f = d.kb_f;
+  a.attn = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1));
+  a.n_units = a.attn.split_start[n] * d.Hkv;
+  a.bar = p.bar();
+  a.gen0 = m->bar_gen;
+  a.err = m->err_dev;
+  m->bar_gen += 4;
+
+  LayerEpis<P, KP> e{};
+  e.qkv.n_rows = n;
+  e.qkv.H = d.H;
+  e.qkv.Hkv = d.Hkv;
+  e.qkv.hd = d.hd;
+  e.qkv.mb = d.mb;
+  e.qkv.dnorm = d.d;
+  e.qkv.eps = d.eps;
+  e.qkv.q = p.q();
+  e.qkv.kc = reinterpret_cast<typename KP::elem*>(p.kc(l));
+  e.qkv.vc = reinterpret_cast<typename KP::elem*>(p.vc(l));
+  e.qkv.bt = p.bt();
+  e.qkv.rope = p.rope();
+  e.qkv.rows = sp;
+  e.o = {n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(2))};
+  e.gu = {n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(3))};
+  e.down = {n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
+
+  const dim3 grid(m->layer_grid);
+  const bool wide = wide_gate_up(d);
+#define SPR_LAYER(HD, JTV, WIDE) k_decode_layer<P, KP, HD, JTV, WIDE><<<grid, 256, 0, m->st>>>(a, e)
+  if (d.hd == 128) {
+    if (JT == 1) wide ? SPR_LAYER(128, 1, true) : SPR_LAYER(128, 1, false);
+    else wide ? SPR_LAYER(128, 2, true) : SPR_LAYER(128, 2, false);
+  } else {
+    if (JT == 1) wide ? SPR_LAYER(64, 1, true) : SPR_LAYER(64, 1, false);
+    else wide ? SPR_LAYER(64, 2, true) : SPR_LAYER(64, 2, false);
+  }
+#undef SPR_LAYER
+  SPR_LAUNCHED(m, "k_decode_layer");
+  return SPR_OK;
+}
+
+// Work-groups per CU of the persistent layer launch: three where every
+// instantiation this model can use fits three (they then run the phases with
+// the per-kernel launch shapes), fewer if not; 0 = unavailable.
+template <class P, class KP, int HD, bool WIDE>
+int layer_grid_per_cu() {
+  int occ = 1 << 30;
+  auto take = [&](const void* k) {
+    int o = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k, 256, 0) != hipSuccess) o = 0;
+    occ = std::min(occ, o);
+  };
+  take(reinterpret_cast<const void*>(&k_decode_layer<P, KP, HD, 1, WIDE>));
+  take(reinterpret_cast<const void*>(&k_decode_layer<P, KP, HD, 2, WIDE>));
+  return std::min(occ, 3);
+}
+template <class P, class KP>
+int layer_grid_per_cu(const spr::Dims& d) {
+  const bool w = wide_gate_up(d);
+  if (d.hd == 128) return w ? layer_grid_per_cu<P, KP, 128, true>() : layer_grid_per_cu<P, KP, 128, false>();
+  return w ? layer_grid_per_cu<P, KP, 64, true>() : layer_grid_per_cu<P, KP, 64, false>();
+}
+
 // One forward pass over rs (rows: slot, position, emitted logits row).
 // tok_in != null: the inputs are tok_in[slot]; otherwise rs.tok.  Emitting
 // rows write their greedy token to tok_out[slot].
@@ -276,8 +418,26 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
   };
   while (count_splits(bpw) > spr::kMaxSplits) ++bpw;
 
+  // A pass of at most 32 rows runs each layer as one persistent launch
+  // (decode mode 1); a timed-out grid barrier of an earlier launch fails the
+  // model here.
+  if (m->err_host != nullptr && *reinterpret_cast<volatile int*>(m->err_host) != 0) {
+    m->sticky = true;
+    return fail(SPR_ERR_HIP, "decode: a persistent layer launch timed out at a grid barrier");
+  }
+  const bool persistent = m->decode_mode == 1 && m->layer_grid > 0 && JT <= 2;
+  // The persistent grid runs the attention work items (flat splits x KV
+  // heads) in one round only if there are at most as many as work-groups:
+  // longer runs per wave instead of a second round.
+  if (persistent)
+    while (count_splits(bpw) * d.Hkv > m->layer_grid && count_splits(bpw) > n) ++bpw;
+
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
+    if (persistent) {
+      if ((st = launch_layer<P, KP>(m, l, rs, sp, JT, bpw)) != SPR_OK) return st;
+      continue;
+    }
     {
       EpiQKV<P, KP> e{};
       e.n_rows = n;
@@ -296,25 +456,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       if ((st = launch_gemm<P>(m, d.nt_qkv, p.wqkv(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
     }
     {
-      AttnArgs a{};
-      a.q = p.q();
-      a.kc = p.kc(l);
-      a.vc = p.vc(l);
-      a.bt = p.bt();
-      a.act = p.act(1);
-      a.part = p.part();
-      a.cnt = p.cnt();
-      a.n_rows = n;
-      a.H = d.H;
-      a.Hkv = d.Hkv;
-      a.G = d.G;
-      a.mb = d.mb;
-      a.bpw = bpw;
-      a.Rp = Rp;
-      a.qscale = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d.hd)));
-      a.rows = sp;
-      a.split_start[0] = 0;
-      for (int r = 0; r < n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw);
+      const AttnArgs a = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1));
       st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a) : launch_attention<P, KP, 64>(m, a);
       if (st != SPR_OK) return st;
     }
@@ -761,6 +903,26 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
   if (e == hipSuccess) e = hipMemsetAsync(p.cnt(), 0, static_cast<size_t>(spr::kMaxRows) * d.Hkv * sizeof(int32_t), m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(1), 0, lay.act_bytes, m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kPrefillRows) * d.d * sizeof(float), m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.act(2), 0, lay.dec_act_bytes, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.act(3), 0, lay.dec_act_bytes, m->st);
+  if (e == hipSuccess) e = hipMemsetAsync(p.bar(), 0, spr::kBarBytes, m->st);
+  // Persistent layer launch: grid = CUs x work-groups per CU, and the
+  // barrier-timeout flag in mapped pinned host memory (zero-copy: the device
+  // writes it only on a timeout, the host reads it before every pass).
+  if (e == hipSuccess && (d.hd == 64 || d.hd == 128)) {
+    const int per_cu = d.dtype == SPR_F32 ? layer_grid_per_cu<F32, F32>(d)
+                       : d.kv_dtype == SPR_BF16 ? layer_grid_per_cu<BF16, BF16>(d)
+                                                : layer_grid_per_cu<BF16, F32>(d);
+    int dev = 0, ncu = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->err_host), sizeof(int), hipHostMallocMapped);
+    if (e == hipSuccess) {
+      *m->err_host = 0;
+      e = hipHostGetDevicePointer(reinterpret_cast<void**>(&m->err_dev), m->err_host, 0);
+    }
+    if (e == hipSuccess && per_cu >= 1) m->layer_grid = per_cu * ncu;
+  }
   if (e == hipSuccess) e = hipStreamSynchronize(m->st);
   if (e != hipSuccess) {
     hip_fail(nullptr, "init", e);
@@ -897,6 +1059,17 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
                                                            which_of[tensor], row0, nrows, out);
   }
   SPR_LAUNCHED(m, "export");
+  return SPR_OK;
+}
+
+spr_status spr_set_decode_mode(spr_model* m, int32_t mode) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (mode != 0 && mode != 1) return fail(SPR_ERR_INVALID_ARG, "set_decode_mode: mode must be 0 or 1");
+  if (mode == 1 && m->layer_grid <= 0)
+    return fail(SPR_ERR_INVALID_ARG, "set_decode_mode: the persistent layer launch is unavailable for this model here");
+  m->decode_mode = mode;
   return SPR_OK;
 }
 
