@@ -52,6 +52,10 @@ __device__ __forceinline__ float2 load_coherent2(const float* p) {
   return make_float2(__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
 }
 
+// Partials the last arriving split reads per round; the host keeps every
+// row's split count within one round.
+constexpr int kMergeChunk = 16;
+
 template <class AP, int HD, bool kCoh>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns);
 
@@ -352,7 +356,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
 // re-read it and are then ignored).
 template <class AP, int HD, bool kCoh>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns) {
-  constexpr int kChunk = 16;
+  constexpr int kChunk = kMergeChunk;
   typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
   const size_t stride = static_cast<size_t>(a.H) * (HD + 4);
   for (int idx = threadIdx.x; idx < a.G * HD; idx += 256) {
