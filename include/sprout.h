@@ -197,6 +197,19 @@ spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows,
 spr_status spr_set_decode_mode(spr_model* m, int32_t mode);
 
 /*
+ * Test aid for the failure path of decode mode 1 (for tests of failure
+ * handling; no other caller needs it): sets how many times a grid barrier of
+ * a persistent layer launch polls before giving up (spin_limit, 64..2^20;
+ * the default is 2^20, about a second), and adds skew to the barrier
+ * generation the next persistent launch waits for.  With skew > 0 that
+ * launch's barriers cannot complete: each wait gives up after spin_limit
+ * polls, the launch still runs to its end (its outputs are meaningless), and
+ * the next call on the model fails with SPR_ERR_HIP.  The model is then
+ * unusable; release it.  SPR_ERR_INVALID_ARG for values out of range.
+ */
+spr_status spr_test_barrier_timeout(spr_model* m, int32_t spin_limit, int32_t skew);
+
+/*
  * Measurement aid: the HBM read ceiling of the projections' load form.
  * Streams every weight matrix a decode step reads (all layers' projections
  * and the LM head, resident in the model's workspace) once per rep with

@@ -88,6 +88,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                       ctypes.POINTER(ctypes.c_float)]
     L.spr_set_decode_mode.restype = ctypes.c_int
     L.spr_set_decode_mode.argtypes = [vp, ctypes.c_int32]
+    L.spr_test_barrier_timeout.restype = ctypes.c_int
+    L.spr_test_barrier_timeout.argtypes = [vp, ctypes.c_int32, ctypes.c_int32]
     L.spr_time_read_ceiling.restype = ctypes.c_int
     L.spr_time_read_ceiling.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_uint64)]
@@ -209,6 +211,10 @@ class DecodeModel:
     def set_decode_mode(self, mode: int):
         """0: one launch per kernel; 1: one persistent launch per layer for passes of at most 32 rows."""
         _check(self.lib.spr_set_decode_mode(self.h, mode))
+
+    def test_barrier_timeout(self, spin_limit: int, skew: int):
+        """Failure-path test aid of decode mode 1 (see spr_test_barrier_timeout)."""
+        _check(self.lib.spr_test_barrier_timeout(self.h, spin_limit, skew))
 
     def read_ceiling(self, reps: int = 5):
         """(GB/s, bytes per pass): plain streaming read of every weight matrix, timed on the model's stream."""

@@ -50,6 +50,7 @@ struct LayerArgs {
   int n_units;            // attention work items: flat splits x KV heads
   unsigned* bar;          // kBarWords words, zero at model start
   unsigned gen0;          // barrier generations gen0 + 1 .. gen0 + 4 are this launch's
+  int spin_limit;         // polls before a barrier gives up (kBarSpinLimit)
   int* err;               // host-visible flag, set when a barrier times out
   AttnArgs attn;
 };
@@ -67,7 +68,7 @@ struct LayerArgs {
 // once it reads gen.  Counts accumulate over launches: counter c holds
 // per_c * gen after barrier gen, so the grid size must not change between
 // launches that share the words.  A wait that has not seen gen after
-// kBarSpinLimit polls, or once another one has timed out, sets *err and lets
+// spin_limit polls, or once another one has timed out, sets *err and lets
 // its work-group through: the launch still ends, and the host reports the
 // failure.
 __device__ __forceinline__ void grid_arrive(unsigned* words, unsigned gen) {
@@ -89,14 +90,14 @@ __device__ __forceinline__ void grid_arrive(unsigned* words, unsigned gen) {
   }
 }
 
-__device__ __forceinline__ void grid_wait(unsigned* words, unsigned gen, int* err) {
+__device__ __forceinline__ void grid_wait(unsigned* words, unsigned gen, int* err, int spin_limit) {
   if (threadIdx.x == 0) {
     const unsigned* rel = words + 64 * (kBarCounters + 1) + 64 * (blockIdx.x % kBarCounters);
     int spins = 0;
     while (static_cast<int>(__hip_atomic_load(rel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - gen) < 0) {
       if ((++spins & 63) == 0) {
         if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0) break;
-        if (spins >= kBarSpinLimit) {
+        if (spins >= spin_limit) {
           __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
           break;
         }
@@ -107,9 +108,9 @@ __device__ __forceinline__ void grid_wait(unsigned* words, unsigned gen, int* er
   __syncthreads();
 }
 
-__device__ __forceinline__ void grid_barrier(unsigned* words, unsigned gen, int* err) {
+__device__ __forceinline__ void grid_barrier(unsigned* words, unsigned gen, int* err, int spin_limit) {
   grid_arrive(words, gen);
-  grid_wait(words, gen, err);
+  grid_wait(words, gen, err, spin_limit);
 }
 
 // One projection over the persistent grid.  kWide: one-wave units of two
@@ -143,7 +144,8 @@ __device__ __forceinline__ void gemm_phase(const uint4* W, const uint4* X, int N
 // wait, so the weight stream is already in flight when the barrier opens.
 template <class P, int JT, bool kWide, class Epi>
 __device__ __forceinline__ void gemm_phase_after(const uint4* W, const uint4* X, int NT, int KB, int Rp, int n_rows,
-                                                 const Epi& epi, float* red, unsigned* bar, unsigned gen, int* err) {
+                                                 const Epi& epi, float* red, unsigned* bar, unsigned gen, int* err,
+                                                 int spin_limit) {
   const int G = gridDim.x;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   constexpr int WAVES = kWide ? 1 : 4, RT = kWide ? 2 : 1;
@@ -154,7 +156,7 @@ __device__ __forceinline__ void gemm_phase_after(const uint4* W, const uint4* X,
   StreamStageOf<P, JT, RT, U> s0, s1;
   grid_arrive(bar, gen);
   if (u0 < nu) stream_prefetch_weights<P, JT, WAVES, RT, U, true>(W, KB, RT * u0, kw, lane, s0, s1);
-  grid_wait(bar, gen, err);
+  grid_wait(bar, gen, err, spin_limit);
   if (u0 < nu)
     stream_gemm_tiles<P, JT, WAVES, Epi, RT, U, true, 2>(W, X, KB, Rp, n_rows, epi, RT * u0, kw, lane, red, s0, s1);
   for (int u = u0 + step; u < nu; u += step) {
@@ -198,13 +200,14 @@ __global__ __launch_bounds__(256, 3) void k_decode_layer(LayerArgs a, LayerEpis<
   __shared__ AttnSmem<HD> sm_attn;
   __shared__ float red[LayerRed<JT>::floats];
   gemm_phase<P, JT, false>(a.wqkv, a.act_in, a.nt_qkv, a.kb_d, a.Rp, a.n_rows, e.qkv, red);
-  grid_barrier(a.bar, a.gen0 + 1, a.err);
+  grid_barrier(a.bar, a.gen0 + 1, a.err, a.spin_limit);
   attn_phase<KP, P, HD>(a.attn, a.n_units, &sm_attn);
-  gemm_phase_after<P, JT, false>(a.wo, a.act_attn, a.nt_o, a.kb_o, a.Rp, a.n_rows, e.o, red, a.bar, a.gen0 + 2, a.err);
+  gemm_phase_after<P, JT, false>(a.wo, a.act_attn, a.nt_o, a.kb_o, a.Rp, a.n_rows, e.o, red, a.bar, a.gen0 + 2, a.err,
+                                 a.spin_limit);
   gemm_phase_after<P, JT, kWideGU>(a.w13, a.act_mid, a.nt_13, a.kb_d, a.Rp, a.n_rows, e.gu, red, a.bar, a.gen0 + 3,
-                                   a.err);
+                                   a.err, a.spin_limit);
   gemm_phase_after<P, JT, false>(a.w2, a.act_h, a.nt_2, a.kb_f, a.Rp, a.n_rows, e.down, red, a.bar, a.gen0 + 4,
-                                 a.err);
+                                 a.err, a.spin_limit);
 }
 
 }  // namespace sprk

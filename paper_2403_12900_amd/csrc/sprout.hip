@@ -57,6 +57,8 @@ struct spr_model {
   int decode_mode = 0;
   int layer_grid = 0;
   unsigned bar_gen = 0;
+  int bar_spin_limit = sprk::kBarSpinLimit;
+  unsigned bar_skew = 0;  // test aid: added to the next launch's barrier generations
   int* err_host = nullptr;
   int* err_dev = nullptr;
   ~spr_model() {
@@ -312,9 +314,11 @@ spr_status launch_layer(spr_model* m, int l, const RowSet& rs, const RowSlotPos&
   a.attn = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1));
   a.n_units = a.attn.split_start[n] * d.Hkv;
   a.bar = p.bar();
-  a.gen0 = m->bar_gen;
+  a.gen0 = m->bar_gen + m->bar_skew;
+  a.spin_limit = m->bar_spin_limit;
   a.err = m->err_dev;
   m->bar_gen += 4;
+  m->bar_skew = 0;
 
   LayerEpis<P, KP> e{};
   e.qkv.n_rows = n;
@@ -1075,6 +1079,17 @@ spr_status spr_set_decode_mode(spr_model* m, int32_t mode) {
   if (mode == 1 && m->layer_grid <= 0)
     return fail(SPR_ERR_INVALID_ARG, "set_decode_mode: the persistent layer launch is unavailable for this model here");
   m->decode_mode = mode;
+  return SPR_OK;
+}
+
+spr_status spr_test_barrier_timeout(spr_model* m, int32_t spin_limit, int32_t skew) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (spin_limit < 64 || spin_limit > sprk::kBarSpinLimit || skew < 0)
+    return fail(SPR_ERR_INVALID_ARG, "test_barrier_timeout: spin_limit in [64, 2^20] and skew >= 0");
+  m->bar_spin_limit = spin_limit;
+  m->bar_skew = static_cast<unsigned>(skew);
   return SPR_OK;
 }
 

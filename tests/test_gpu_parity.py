@@ -178,6 +178,30 @@ def test_persistent_layer_equals_per_kernel_7b():
     b.close()
 
 
+def test_persistent_layer_barrier_timeout_fails_the_next_call():
+    """A persistent launch whose grid barriers cannot complete (forced from the host: its barrier generation is
+    shifted and the poll limit cut to 64) still ends, and the next call on the model reports the timeout."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel, SproutError, SPR_ERR_HIP, SPR_ERR_INVALID_ARG
+    m, _, _ = TOY_CASES["bf16_mha_hd64_ragged"]
+    dm = DecodeModel(m, 78, max_slots=2, max_ctx=64)
+    dm.set_decode_mode(1)
+    tok = dm.new_token_buffer()
+    rng = np.random.default_rng(3)
+    dm.prefill([0, 1], _prompts(rng, m.vocab, [9, 20]), [6, 6], tok)
+    with pytest.raises(SproutError) as bad:
+        dm.test_barrier_timeout(8, 1)
+    assert bad.value.status == SPR_ERR_INVALID_ARG
+    dm.decode_step([0, 1], [9, 20], tok)                  # healthy
+    dm.test_barrier_timeout(64, 1000)
+    dm.decode_step([0, 1], [10, 21], tok)                 # enqueued; its barriers give up after 64 polls
+    torch.cuda.synchronize()
+    with pytest.raises(SproutError) as failed:
+        dm.decode_step([0, 1], [11, 22], tok)
+    assert failed.value.status == SPR_ERR_HIP and "grid barrier" in str(failed.value)
+    dm.close()
+
+
 def test_forced_tokens_and_in_place_buffer():
     """Teacher forcing through the device token buffer equals the oracle fed the same tokens."""
     m, plens, stops = TOY_CASES["bf16_mha_hd64_ragged"]
