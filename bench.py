@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "decode tokens/s + achieved HBM GB/s, Llama-2-7B-shape bf16, ragged batch 32"
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
-DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16>, 2, 8, true>"
+DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16, false>, 2, 8, true>"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_gemm_pmc_llama2_7b_b8.txt")
 
 
