@@ -88,6 +88,22 @@ def traffic_probe():
     log(f"traffic probe: 4 device copies of {PMC_COPY_BYTES} bytes")
 
 
+def pmc_probe():
+    """Kernels for a rocprofv3 --pmc diagnosis of the projections' memory path: the dominant gate/up
+    kernel, the O projection (fewest row tiles) and the plain weight stream of the read ceiling."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    cfg = CONFIGS["c3"]
+    model = DecodeModel(cfg.model, cfg.weight_seed, max_slots=32, max_ctx=256, kv_blocks=64)
+    model.time_projection("gate_up", 8, 32)
+    model.time_projection("o", 8, 32)
+    model.read_ceiling(2)
+    torch.cuda.synchronize()
+    log("pmc probe: 32 gate/up, 32 O, 2 read-ceiling passes")
+    model.close()
+
+
 def _pmc_rows(path: str, counter: str):
     """(kernel name, value) per dispatch from a rocprofv3 counter_collection.csv."""
     import csv
@@ -309,6 +325,8 @@ def main():
     ap.add_argument("--no-serving", action="store_true", help="skip the continuous-batching measurement")
     ap.add_argument("--decode-mode", type=int, default=None,
                     help="0: one launch per kernel; 1: one persistent launch per layer (default: the library's)")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="run 32 gate/up and 32 O projections at 8 rows and 2 read-ceiling passes, for rocprofv3 --pmc")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only launch the dominant kernel and a calibration copy (for rocprofv3 --pmc)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -316,6 +334,9 @@ def main():
     args = ap.parse_args()
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary)
+        return
+    if args.pmc_probe:
+        pmc_probe()
         return
     if args.traffic_probe:
         traffic_probe()
