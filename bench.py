@@ -14,7 +14,6 @@ it.
 Prints one JSON line on stdout (progress goes to stderr).
 """
 import argparse
-import glob
 import hashlib
 import json
 import os
@@ -37,9 +36,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# The sources that define the dominant kernel (its template arguments fix its launch shape).
+DOMINANT_SOURCES = ("device_common.h", "gemm_kernels.h")
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2403_12900_amd", "csrc", "*"))):
+    for f in (os.path.join(ROOT, "paper_2403_12900_amd", "csrc", n) for n in DOMINANT_SOURCES):
         with open(f, "rb") as fh:
             h.update(os.path.basename(f).encode())
             h.update(fh.read())
@@ -48,7 +51,7 @@ def kernel_source_hash() -> str:
 
 def measured_traffic(bytes_per_launch: float):
     """HBM bytes per launch of the dominant kernel from the committed PMC summary,
-    or None when the kernel sources changed since the counters were taken."""
+    or None when its sources (DOMINANT_SOURCES) changed since the counters were taken."""
     if not os.path.exists(TRAFFIC_PROFILE):
         return None
     vals = {}
@@ -147,6 +150,7 @@ def traffic_summary(fetch_csv: str, write_csv: str) -> None:
 #   python3 /root/repo/bench.py --traffic-summary /tmp/pmc_fetch/probe_counter_collection.csv /tmp/pmc_write/probe_counter_collection.csv
 # Each counter (KiB per dispatch) is scaled by the ratio true/measured of the same counter on a
 # plain device copy of {PMC_COPY_BYTES} bytes (reads and writes that many bytes).
+# kernel_source_hash covers the kernel's sources: csrc/{' and csrc/'.join(DOMINANT_SOURCES)}.
 kernel = {DOMINANT}
 dispatches_fetch = {n_fetch}
 dispatches_write = {n_write}

@@ -2,10 +2,12 @@
 // decode pass -- QKV projection (RMSNorm, RoPE, KV append), attention, O
 // projection (+ residual), gate/up projection (RMSNorm, SwiGLU), down
 // projection (+ residual) -- in one launch of G resident work-groups, with a
-// grid barrier between phases instead of a kernel boundary.  Each phase maps
-// its work onto the work-groups exactly as the per-kernel path's launch shape
-// would (see gemm_phase), so the difference is only what a kernel boundary
-// costs: the drain and refill of the whole chip, about 2.5 us per launch.
+// grid barrier between phases instead of a kernel boundary.  The projection
+// phases use the per-kernel path's launch shapes (four-wave one-tile units;
+// one-wave two-tile units for a wide gate/up), except that QKV at 17-32 rows
+// keeps one-tile units where the per-kernel path pairs tiles; the attention
+// splits are fitted to the grid so they run in one round.  The phases after a
+// barrier issue their first weight loads while the barrier completes.
 //
 // Coherence inside the launch (the XCDs' L2 caches are not coherent with one
 // another, and no release fence is used):
