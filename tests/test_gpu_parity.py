@@ -202,6 +202,41 @@ def test_persistent_layer_barrier_timeout_fails_the_next_call():
     dm.close()
 
 
+def test_fragmented_kv_reservation():
+    """Paged KV with a fragmented reservation: slots 0-2 reserve blocks [0,1], [2,3], [4,5]; slot 1 is
+    freed and refilled with a longer prompt, which reserves [2,3,6,7].  Teacher-forced logits of all three
+    rows match the oracle."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    m, _, _ = TOY_CASES["bf16_mha_hd64_ragged"]
+    say("fragmented KV reservation")
+    rng = np.random.default_rng(9)
+    dm = DecodeModel(m, 78, max_slots=3, max_ctx=96, kv_blocks=12)
+    tok = dm.new_token_buffer()
+    first = _prompts(rng, m.vocab, [20, 20, 20])
+    dm.prefill([0, 1, 2], first, [4, 4, 4], tok)
+    dm.free_slot(1)
+    longer = _prompts(rng, m.vocab, [50])[0]
+    dm.prefill([1], [longer], [4], tok)
+    assert dm.lib.spr_free_blocks(dm.h) == 12 - 8
+    prompts = [first[0], longer, first[2]]
+    forced = rng.integers(0, m.vocab, size=(3, 3)).astype(np.int32)
+    lens = [20, 50, 20]
+    got = []
+    for s in range(3):
+        tok.copy_(torch.from_numpy(forced[s]).to(tok.device))
+        lg, _ = dm.decode_step([0, 1, 2], lens, tok, want_logits=True)
+        got.append(lg.cpu().numpy())
+        lens = [l + 1 for l in lens]
+    w = R.Weights(oracle_shape(m), 78)
+    for i in range(3):
+        ref = R.forward_causal(w, list(prompts[i]) + forced[:, i].tolist(), [len(prompts[i]) + s for s in range(3)])
+        for s in range(3):
+            d = np.abs(got[s][i] - ref[s]).max()
+            assert d <= BF16_TOL[0], (i, s, d)
+    dm.close()
+
+
 def test_forced_tokens_and_in_place_buffer():
     """Teacher forcing through the device token buffer equals the oracle fed the same tokens."""
     m, plens, stops = TOY_CASES["bf16_mha_hd64_ragged"]
