@@ -322,7 +322,7 @@ def cpu_baseline(cfg, wl, seconds: float):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
@@ -393,15 +393,19 @@ def main():
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # One event pair brackets all timed steps (the reported mean); events between steps give each
+    # step's own time for the median.
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     wall0 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
+    marks[0].record()
+    for k in range(args.steps):
         one_step()
-    e1.record()
+        marks[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = marks[0].elapsed_time(marks[-1]) / args.steps
+    per_step = [marks[k].elapsed_time(marks[k + 1]) for k in range(args.steps)]
+    ms_median = float(np.median(per_step))
     tokens = st["decode_tokens"]
     value = tokens / (ms / 1e3)
     gbps = st["bytes"] / (ms / 1e3) / 1e9
@@ -433,6 +437,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
+        "ms_per_step_median": round(ms_median, 3),
+        "ms_per_step_runs": [round(x, 1) for x in per_step],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
