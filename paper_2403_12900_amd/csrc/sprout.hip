@@ -56,6 +56,8 @@ struct spr_model {
   // mapped pinned host memory (host and device views).
   int decode_mode = 0;
   int layer_grid = 0;
+  // Decode attention work-groups resident at once (CUs x occupancy).
+  int attn_slots = 1024;
   unsigned bar_gen = 0;
   int bar_spin_limit = sprk::kBarSpinLimit;
   unsigned bar_skew = 0;  // test aid: added to the next launch's barrier generations
@@ -375,6 +377,16 @@ int layer_grid_per_cu(const spr::Dims& d) {
   return w ? layer_grid_per_cu<P, KP, 64, true>() : layer_grid_per_cu<P, KP, 64, false>();
 }
 
+// Decode attention work-groups resident per CU (0 = unavailable).
+template <class P, class KP>
+int attn_blocks_per_cu(const spr::Dims& d) {
+  int o = 0;
+  const void* k = d.hd == 128 ? reinterpret_cast<const void*>(&k_attn_decode<KP, P, 128>)
+                              : reinterpret_cast<const void*>(&k_attn_decode<KP, P, 64>);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k, 256, 0) != hipSuccess) o = 0;
+  return o;
+}
+
 // One forward pass over rs (rows: slot, position, emitted logits row).
 // tok_in != null: the inputs are tok_in[slot]; otherwise rs.tok.  Emitting
 // rows write their greedy token to tok_out[slot].
@@ -409,17 +421,27 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
 
   // KV splits: a work-group covers 4 * bpw blocks of one (row, KV head), a
   // run of bpw blocks per wave.  bpw stays 1 until the pass has more blocks
-  // than about 4096 waves (16 per CU, the kernel's occupancy) take at once,
-  // and grows further only while the splits exceed the partial buffer.
+  // than the resident waves (4 per work-group) take at once.  Rounding each
+  // row up to whole splits can still leave more work-groups than stay
+  // resident; then runs up to twice as long per wave that fit them into one
+  // round are taken (measured on 7B, 12-28 rows of 400 positions: 3-15 us
+  // less per layer), but not longer ones (a batch whose longest row would
+  // need them: one long run then sets the time).  bpw grows further only
+  // while the splits exceed the partial buffer.
   int total_blk = 0;
   for (int r = 0; r < n; ++r) total_blk += (rs.pos[r] + 1 + 15) / 16;
-  int bpw = ceil_div(total_blk * d.Hkv, 4096);
+  int bpw = ceil_div(total_blk * d.Hkv, 4 * m->attn_slots);
   if (bpw < 1) bpw = 1;
   auto count_splits = [&](int w) {
     int t = 0;
     for (int r = 0; r < n; ++r) t += ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * w);
     return t;
   };
+  {
+    int fit = bpw;
+    while (count_splits(fit) * d.Hkv > m->attn_slots && count_splits(fit) > n && fit < 2 * bpw) ++fit;
+    if (count_splits(fit) * d.Hkv <= m->attn_slots) bpw = fit;
+  }
   while (count_splits(bpw) > spr::kMaxSplits) ++bpw;
   // A row's splits are merged by its last arriving split, kMergeChunk
   // partials per round of loads: keep every row within one round (measured
@@ -931,6 +953,10 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
       e = hipHostGetDevicePointer(reinterpret_cast<void**>(&m->err_dev), m->err_host, 0);
     }
     if (e == hipSuccess && per_cu >= 1) m->layer_grid = per_cu * ncu;
+    const int attn_per_cu = d.dtype == SPR_F32 ? attn_blocks_per_cu<F32, F32>(d)
+                            : d.kv_dtype == SPR_BF16 ? attn_blocks_per_cu<BF16, BF16>(d)
+                                                     : attn_blocks_per_cu<BF16, F32>(d);
+    if (e == hipSuccess && attn_per_cu >= 1) m->attn_slots = attn_per_cu * ncu;
   }
   if (e == hipSuccess) e = hipStreamSynchronize(m->st);
   if (e != hipSuccess) {
