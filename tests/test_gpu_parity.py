@@ -112,6 +112,12 @@ TOY_CASES = {
     "bf16_long_context_splits": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=128, vocab=500),
         [700, 300], [20, 3]),
+    # 32 KV heads x 24 rows of 141-147 positions: two splits per row would be 1536 attention
+    # work-groups, more than the 1024 resident on MI355X, so the pass takes three-block runs per wave
+    # and one split per row.
+    "bf16_mha32_splits_fit_resident": (
+        ModelConfig(n_layers=1, d_model=256, n_heads=32, n_kv_heads=32, head_dim=64, d_ff=128, vocab=300),
+        [140 + (i % 5) for i in range(24)], [3] * 24),
     # Prompts spanning prefill chunks (1024 rows): 1500 crosses the first boundary, 700 the second.
     "bf16_prompts_across_chunks": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
