@@ -80,8 +80,11 @@ __device__ __forceinline__ float gram_diagonal(const f32x4_t& gm, int lane) {
 // issues the next stage of UH K-blocks before computing the current one, so
 // its requests stay in flight while it computes.  For epilogues that apply
 // RMSNorm, the rows' sums of squares come from MFMA too: the Gram product
-// X^T X of each activation fragment with itself (hi.hi + hi.lo + lo.hi)
-// has them on its diagonal.
+// X^T X of each activation fragment with itself has them on its diagonal.
+// For bf16 activations only the hi parts enter it (one MFMA, not three): with
+// x = hi + lo and |lo| <= 2^-9 |x|, the dropped terms 2 hi lo + lo^2 move the
+// sum by at most 2^-8 of itself, and by about 2^-8 / sqrt(K) for rounding
+// errors of random sign, so the RMSNorm scale moves by half that.
 // LDS floats the cross-wave reduction of stream_gemm_tiles needs.
 template <int JT, int WAVES, int RT>
 struct StreamRed {
@@ -187,13 +190,7 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
         for (int t = 0; t < RT; ++t)
 #pragma unroll
           for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[u][t], st.x[u][j][q]);
-        if constexpr (Epi::kNorm) {
-          gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
-          if constexpr (PARTS == 2) {
-            gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][1]);
-            gram[j] = P::mma(gram[j], st.x[u][j][1], st.x[u][j][0]);
-          }
-        }
+        if constexpr (Epi::kNorm) gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
       }
     }
   };
@@ -227,13 +224,7 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
       for (int t = 0; t < RT; ++t)
 #pragma unroll
         for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[0][t], st.x[0][j][q]);
-      if constexpr (Epi::kNorm) {
-        gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
-        if constexpr (PARTS == 2) {
-          gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][1]);
-          gram[j] = P::mma(gram[j], st.x[0][j][1], st.x[0][j][0]);
-        }
-      }
+      if constexpr (Epi::kNorm) gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
     }
   }
   float ssq[JT];
