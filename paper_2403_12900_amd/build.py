@@ -17,6 +17,9 @@ HIP_FLAGS = [
     # MFMA accumulators in VGPRs: epilogues and the softmax rescale operate on
     # them with VALU instructions, which cannot address AGPRs.
     "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # The leading scalar kernel arguments (pointers, sizes) arrive preloaded in
+    # SGPRs, so a kernel's first loads need not wait for its argument fetch.
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Wno-unused-result",
 ]
 
