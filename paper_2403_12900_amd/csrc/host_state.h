@@ -17,7 +17,11 @@ namespace spr {
 constexpr int kKvBlock = 16;     // positions per KV block
 constexpr int kBarBytes = 4 * 64 * (2 * 32 + 1);  // grid barrier words of the persistent layer launch
 constexpr int kMaxRows = 128;    // token rows per decode pass (and LM-head rows of a prefill chunk)
-constexpr int kPrefillRows = 1024;  // token rows per prefill chunk
+// Token rows per prefill chunk.  Chunks fill up in request order.  At 7B
+// shapes, 32 prompts of 8427 tokens in all ran 14% faster in 4096-row chunks
+// than in 1024-row ones (more work-groups per projection), and 2% faster than
+// in three equal chunks.
+constexpr int kPrefillRows = 4096;
 constexpr int kPrefillTiles = kPrefillRows / 16 + 64;  // attention query tiles per chunk (segments add one each)
 constexpr int kMaxSplits = 2048; // KV splits over all rows of one pass (decode attention)
 constexpr int kFragBytes = 1024; // one MFMA operand fragment: 64 lanes x 16 bytes

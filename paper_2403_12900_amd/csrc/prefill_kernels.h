@@ -12,7 +12,7 @@
 
 namespace sprk {
 
-constexpr int kPrefillRows = 1024;  // token rows per prefill chunk
+constexpr int kPrefillRows = 4096;  // token rows per prefill chunk
 
 // One token row of a chunk.
 struct PrefillRow {

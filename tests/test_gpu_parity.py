@@ -118,10 +118,11 @@ TOY_CASES = {
     "bf16_mha32_splits_fit_resident": (
         ModelConfig(n_layers=1, d_model=256, n_heads=32, n_kv_heads=32, head_dim=64, d_ff=128, vocab=300),
         [140 + (i % 5) for i in range(24)], [3] * 24),
-    # Prompts spanning prefill chunks (1024 rows): 1500 crosses the first boundary, 700 the second.
+    # A prompt spanning prefill chunks: 7347 rows run as chunks of 4096 and 3251 rows, and the
+    # 2500-row prompt crosses the boundary at its row 1089.
     "bf16_prompts_across_chunks": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
-        [1500, 7, 700, 40], [3, 4, 2, 5]),
+        [3000, 7, 2500, 40, 1800], [3, 4, 2, 5, 3]),
 }
 
 
