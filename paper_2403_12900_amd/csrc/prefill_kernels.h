@@ -97,7 +97,7 @@ __device__ __forceinline__ void lds_stage_barrier() {
 
 // Tiled projection: out[b][n] = sum_k W[n][k] x[b][k] for rows b < M, fused
 // with the op that follows (Epi).  A work-group computes TN weight tiles (16
-// output features each) x TM row tiles (16 rows each) with four waves, each
+// output features each) x TM row tiles (16 rows each) with NW waves, each
 // owning a WN x WM block of 16 x 16 MFMA tiles.  Per K-block the work-group's
 // operands -- TN weight fragments and TM x parts activation fragments, 1 KiB
 // each -- go from global memory straight into LDS (global_load_lds, no
@@ -107,23 +107,27 @@ __device__ __forceinline__ void lds_stage_barrier() {
 // loads on its own) keep two K-blocks in flight; each K-block costs one
 // barrier: wait for its own loads, barrier (which also frees the stage read
 // one K-block earlier), issue the loads two K-blocks ahead, multiply.  Weight
-// tiles past NT re-read tile NT - 1 and are not stored.
-template <int TN, int TM>
+// tiles past NT re-read tile NT - 1 and row tiles past Rp re-read the last
+// one; neither is stored.
+// The operands a K-block moves from L2 into LDS, TN + parts x TM fragments,
+// bound these kernels before MFMA does: the largest shape (256 features x 256
+// rows, eight waves) moves half the bytes per product of 128 x 128.
+template <int TN, int TM, int NW>
 struct TileShape {
-  static constexpr int GN = TN == 4 && TM == 8 ? 1 : 2;  // waves along features
-  static constexpr int GM = 4 / GN;                     // waves along rows
+  static constexpr int GN = NW == 8 ? 2 : TN == 4 && TM == 8 ? 1 : 2;  // waves along features
+  static constexpr int GM = NW / GN;                                  // waves along rows
   static constexpr int WN = TN / GN, WM = TM / GM;
-  static_assert(GN * GM == 4 && WN * GN == TN && WM * GM == TM, "tile shape");
+  static_assert(GN * GM == NW && WN * GN == TN && WM * GM == TM, "tile shape");
 };
 
-template <class P, int TN, int TM, class Epi>
-__global__ __launch_bounds__(256) void k_tile_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X, int NT,
-                                                   int KB, int Rp, Epi epi) {
+template <class P, int TN, int TM, class Epi, int NW = 4>
+__global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X,
+                                                       int NT, int KB, int Rp, Epi epi) {
   constexpr int PARTS = P::parts;
   constexpr int NFRAG = TN + TM * PARTS;
-  static_assert(NFRAG % 4 == 0, "fragments per stage must split over four waves");
-  constexpr int L = NFRAG / 4;  // loads per wave per stage
-  using TS = TileShape<TN, TM>;
+  static_assert(NFRAG % NW == 0, "fragments per stage must split over the waves");
+  constexpr int L = NFRAG / NW;  // loads per wave per stage
+  using TS = TileShape<TN, TM, NW>;
   constexpr int WN = TS::WN, WM = TS::WM;
   __shared__ uint4 st0[NFRAG][64];
   __shared__ uint4 st1[NFRAG][64];
@@ -138,14 +142,15 @@ __global__ __launch_bounds__(256) void k_tile_gemm(const uint4* __restrict__ W, 
   auto issue = [&](int kb, uint4(*dst)[64]) {
 #pragma unroll
     for (int i = 0; i < L; ++i) {
-      const int f = wave + 4 * i;
+      const int f = wave + NW * i;
       const uint4* src;
       if (f < TN) {
         const int nt = min(nt0 + f, NT - 1);
         src = W + (static_cast<size_t>(nt) * KB + kb) * 64 + lane;
       } else {
         const int a = f - TN, q = a / TM, tt = a % TM;
-        src = X + (static_cast<size_t>(kb) * PARTS + q) * xpart + static_cast<size_t>(m0 + 16 * tt) * 4 + xlane;
+        const int r0 = min(m0 + 16 * tt, Rp - 16);
+        src = X + (static_cast<size_t>(kb) * PARTS + q) * xpart + static_cast<size_t>(r0) * 4 + xlane;
       }
       __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)&dst[f][0], 16, 0, 0);
     }
