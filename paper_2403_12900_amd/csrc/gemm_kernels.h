@@ -81,10 +81,9 @@ __device__ __forceinline__ float gram_diagonal(const f32x4_t& gm, int lane) {
 // its requests stay in flight while it computes.  For epilogues that apply
 // RMSNorm, the rows' sums of squares come from MFMA too: the Gram product
 // X^T X of each activation fragment with itself has them on its diagonal.
-// For bf16 activations only the hi parts enter it (one MFMA, not three): with
-// x = hi + lo and |lo| <= 2^-9 |x|, the dropped terms 2 hi lo + lo^2 move the
-// sum by at most 2^-8 of itself, and by about 2^-8 / sqrt(K) for rounding
-// errors of random sign, so the RMSNorm scale moves by half that.
+// For bf16 activations (x = hi + lo) that is hi.hi + 2 hi.lo, two MFMAs: the
+// diagonal of hi.lo equals that of lo.hi, and lo.lo (at most 2^-18 of the
+// sum) is left out.
 // LDS floats the cross-wave reduction of stream_gemm_tiles needs.
 template <int JT, int WAVES, int RT>
 struct StreamRed {
@@ -134,12 +133,13 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
   constexpr int UH = U / 2 > 0 ? U / 2 : 1;
   using Stage = StreamStageOf<P, JT, RT, U>;
   const int kb0 = (KB * wave) / WAVES, kb1 = (KB * (wave + 1)) / WAVES;
-  f32x4_t acc[RT][JT], gram[JT];
+  f32x4_t acc[RT][JT], gram[JT], gram_hl[JT];
 #pragma unroll
   for (int j = 0; j < JT; ++j) {
 #pragma unroll
     for (int t = 0; t < RT; ++t) acc[t][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     gram[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    gram_hl[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   const uint4* wp = W + static_cast<size_t>(nt0) * KB * 64 + lane;
   const size_t wtile = static_cast<size_t>(KB) * 64;  // uint4 per row tile
@@ -190,7 +190,10 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
         for (int t = 0; t < RT; ++t)
 #pragma unroll
           for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[u][t], st.x[u][j][q]);
-        if constexpr (Epi::kNorm) gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
+        if constexpr (Epi::kNorm) {
+          gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
+          if constexpr (PARTS == 2) gram_hl[j] = P::mma(gram_hl[j], st.x[u][j][0], st.x[u][j][1]);
+        }
       }
     }
   };
@@ -224,12 +227,17 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
       for (int t = 0; t < RT; ++t)
 #pragma unroll
         for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[0][t], st.x[0][j][q]);
-      if constexpr (Epi::kNorm) gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
+      if constexpr (Epi::kNorm) {
+        gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
+        if constexpr (PARTS == 2) gram_hl[j] = P::mma(gram_hl[j], st.x[0][j][0], st.x[0][j][1]);
+      }
     }
   }
   float ssq[JT];
 #pragma unroll
-  for (int j = 0; j < JT; ++j) ssq[j] = Epi::kNorm ? gram_diagonal(gram[j], lane) : 0.f;
+  for (int j = 0; j < JT; ++j)
+    ssq[j] = Epi::kNorm ? gram_diagonal(gram[j], lane) + (PARTS == 2 ? 2.f * gram_diagonal(gram_hl[j], lane) : 0.f)
+                        : 0.f;
   if constexpr (WAVES > 1) {
     // red[w - 1][j][4 t + c][lane], then the sums of squares at [.][j][4 RT][lane].
     auto at = [&](int w, int j, int i) -> float& { return red[((w * JT + j) * (4 * RT + 1) + i) * 64 + lane]; };
