@@ -107,6 +107,31 @@ def pmc_probe():
     model.close()
 
 
+def prefill_probe():
+    """The c3 batch's prefill (8427 prompt tokens: chunks of 4096, 4096 and 235 rows), run twice,
+    for a rocprofv3 --pmc diagnosis of the prefill GEMMs."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    from paper_2403_12900_amd.workload import make_workload
+    cfg = CONFIGS["c3"]
+    wl = make_workload(cfg)
+    seq = [int(x) for x in wl.seq_lens]
+    stops = [int(x) for x in wl.stop_lens]
+    max_ctx = max(s + L - 1 for s, L in zip(seq, stops))
+    blocks = sum((s + L - 1 + 15) // 16 for s, L in zip(seq, stops))
+    model = DecodeModel(cfg.model, cfg.weight_seed, max_slots=wl.batch, max_ctx=max_ctx, kv_blocks=blocks)
+    tok = model.new_token_buffer()
+    for k in range(2):
+        if k:
+            for i in range(wl.batch):
+                model.free_slot(i)
+        model.prefill(list(range(wl.batch)), wl.tokens, stops, tok)
+    torch.cuda.synchronize()
+    log(f"prefill probe: 2 prefills of {sum(seq)} prompt tokens")
+    model.close()
+
+
 def _pmc_rows(path: str, counter: str):
     """(kernel name, value) per dispatch from a rocprofv3 counter_collection.csv."""
     import csv
@@ -331,6 +356,8 @@ def main():
                     help="0: one launch per kernel; 1: one persistent launch per layer (default: the library's)")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 32 gate/up and 32 O projections at 8 rows and 2 read-ceiling passes, for rocprofv3 --pmc")
+    ap.add_argument("--prefill-probe", action="store_true",
+                    help="only run the c3 prefill twice (for rocprofv3 --pmc of the prefill GEMMs)")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only launch the dominant kernel and a calibration copy (for rocprofv3 --pmc)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -344,6 +371,9 @@ def main():
         return
     if args.traffic_probe:
         traffic_probe()
+        return
+    if args.prefill_probe:
+        prefill_probe()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the decode path runs one model "
