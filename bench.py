@@ -132,6 +132,45 @@ def prefill_probe():
     model.close()
 
 
+def step_sweep(key: str, steps: int = 12):
+    """Decode-step time and algorithmic GB/s of one configuration's model at 1, 8, 16 and 32 rows of
+    about 512 cached positions: the weights of every layer and the LM head, plus each row's KV read
+    (its cached positions and the new one) and write."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    cfg = CONFIGS[key]
+    m = cfg.model
+    dm = DecodeModel(m, cfg.weight_seed, max_slots=32, max_ctx=512 + steps + 2, kv_blocks=32 * 34)
+    tok = dm.new_token_buffer()
+    rng = np.random.default_rng(0)
+    wbytes = m.weight_elements_per_step() * m.weight_bytes
+    kv_tok = m.kv_bytes_per_token()
+    for rows in (1, 8, 16, 32):
+        slots = list(range(rows))
+        dm.prefill(slots, [rng.integers(0, m.vocab, size=512).astype(np.int32) for _ in range(rows)],
+                   [steps + 2] * rows, tok)
+        lens = [512] * rows
+        dm.decode_step(slots, lens, tok)
+        lens = [x + 1 for x in lens]
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            dm.decode_step(slots, lens, tok)
+            lens = [x + 1 for x in lens]
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        cached = 513 + (steps - 1) / 2         # mean cached positions per row over the timed steps
+        byts = wbytes + rows * (cached + 2) * kv_tok
+        log(f"{cfg.name} rows {rows:2d}: {ms:.3f} ms/step, {rows / ms * 1e3:.0f} tokens/s, "
+            f"{byts / ms / 1e6:.0f} GB/s algorithmic ({byts / ms / 1e6 / PEAK_HBM_GBPS * 100:.1f}% of 8 TB/s)")
+        for sl in slots:
+            dm.free_slot(sl)
+    dm.close()
+
+
 def _pmc_rows(path: str, counter: str):
     """(kernel name, value) per dispatch from a rocprofv3 counter_collection.csv."""
     import csv
@@ -356,6 +395,8 @@ def main():
                     help="0: one launch per kernel; 1: one persistent launch per layer (default: the library's)")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 32 gate/up and 32 O projections at 8 rows and 2 read-ceiling passes, for rocprofv3 --pmc")
+    ap.add_argument("--step-sweep", metavar="CONFIG", default=None,
+                    help="decode-step GB/s of one configuration's model (c2..c5) at 1-32 rows of ~512 positions")
     ap.add_argument("--prefill-probe", action="store_true",
                     help="only run the c3 prefill twice (for rocprofv3 --pmc of the prefill GEMMs)")
     ap.add_argument("--traffic-probe", action="store_true",
@@ -374,6 +415,9 @@ def main():
         return
     if args.prefill_probe:
         prefill_probe()
+        return
+    if args.step_sweep:
+        step_sweep(args.step_sweep)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the decode path runs one model "
