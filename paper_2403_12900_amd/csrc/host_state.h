@@ -22,7 +22,7 @@ constexpr int kMaxRows = 128;    // token rows per decode pass (and LM-head rows
 // than in 1024-row ones (more work-groups per projection), and 2% faster than
 // in three equal chunks.
 constexpr int kPrefillRows = 4096;
-constexpr int kPrefillTiles = kPrefillRows / 16 + 64;  // attention query tiles per chunk (segments add one each)
+constexpr int kPrefillTiles = kPrefillRows / 16 + 64;  // attention query tiles per chunk, 64 rows or fewer each
 constexpr int kMaxSplits = 2048; // KV splits over all rows of one pass (decode attention)
 constexpr int kFragBytes = 1024; // one MFMA operand fragment: 64 lanes x 16 bytes
 

@@ -19,7 +19,7 @@ struct PrefillRow {
   int slot, pos, tok, pad;
 };
 
-// Up to 16 consecutive rows of one request (positions pos0 .. pos0 + n - 1
+// Up to 64 consecutive rows of one request (positions pos0 .. pos0 + n - 1
 // at chunk rows row0 .. row0 + n - 1): one attention query tile.
 struct PrefillTile {
   int slot, row0, n, pos0;
@@ -307,14 +307,17 @@ struct EpiSwiGLURows {
   }
 };
 
-// Causal attention over each query tile's own request.  Work-group (tile,
-// query head): the tile's 16 rows are the MFMA columns, the KV blocks up to
-// the tile's last position are split into four contiguous runs, one per wave,
-// merged through LDS as in decode.  Column c (position pos0 + c) sees
-// positions <= pos0 + c; columns past the tile's rows repeat its last row and
-// are not stored.  A wave whose run lies wholly after a column's position
-// keeps that column at m = -inf, l = 0 and weighs 0 in the merge (wave 0's run
-// starts at position 0, so every column's merged maximum is finite).
+// Causal attention over each query tile's own request.  Work-group (tile of
+// up to 64 consecutive rows of one request, query head): wave w owns rows
+// 16 w .. 16 w + 15 as its 16 MFMA columns.  The work-group walks the KV blocks
+// up to the tile's last position once.  Each block's K and V tiles come from
+// global memory once, straight into LDS, and all four waves multiply their
+// columns against them; the next block's loads are in flight while the
+// current one is used (two LDS buffers, two barriers per block).  Sharing a
+// block among 64 queries instead of 16 cuts the cache reads that bound this
+// kernel fourfold.  A wave skips blocks that start after its last position;
+// block 0 holds position 0, so every column's running maximum is finite after
+// it.  Columns past the tile's rows repeat its last row and are not stored.
 template <class P, class AP, int HD>
 __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ q, const void* kcv, const void* vcv,
                                                       const int32_t* __restrict__ bt,
@@ -323,21 +326,44 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   using E = typename P::elem;
   using Blk = KVBlock<P, HD>;
   constexpr bool kBf16 = sizeof(E) == 2;
-  constexpr int NF = Blk::NF;
+  constexpr int NF = Blk::NF, NV = Blk::NV;
   constexpr int NE = HD / 16;
-  constexpr int EPW = NE / 4;
+  constexpr int KU = NF * 64, KVU = (NF + NV) * 64;  // uint4 of a block's K tile, of its K and V tiles
+  constexpr int PER = KVU / 256;                     // uint4 each thread stages per block
+  static_assert(KVU % 256 == 0, "a block's K and V tiles split evenly over the work-group");
+  __shared__ uint4 skv[2][KVU];
   const PrefillTile tile = tiles[blockIdx.x];
   const int hq = blockIdx.y, kvh = hq / (H / Hkv);
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
-  const int cq = c < tile.n ? c : tile.n - 1;
-  const int pc = tile.pos0 + cq;                 // this column's position
+  const int r0 = 16 * wave;                            // the wave's first row of the tile
+  const int rw = min(16, tile.n - r0);                 // its rows (none if <= 0)
+  const int cq = rw > 0 ? r0 + (c < rw ? c : rw - 1) : tile.n - 1;
+  const int pc = tile.pos0 + cq;                       // this column's position
+  const int wave_last = tile.pos0 + (rw > 0 ? r0 + rw - 1 : 0);
   const int max_pos = tile.pos0 + tile.n - 1;
   const int nblk = (max_pos >> 4) + 1;
-  const int lo = nblk * wave / 4, hi = nblk * (wave + 1) / 4;
   const int32_t* btrow = bt + static_cast<size_t>(tile.slot) * mb;
-  int ids = lo + lane < hi ? btrow[lo + lane] : 0;
+  const E* kc = static_cast<const E*>(kcv);
+  const E* vc = static_cast<const E*>(vcv);
+  int ids = lane < nblk ? btrow[lane] : 0;             // block ids of blocks [i0, i0 + 64)
+
+  // Block i's K and V tiles, straight from global memory into LDS buffer buf
+  // (global_load_lds; no registers), thread t moving uint4 t, t + 256, ...
+  // The block's id is lane (i mod 64) of ids.
+  auto issue = [&](int i, int buf) __attribute__((always_inline)) {
+    const int blk = __builtin_amdgcn_readlane(ids, i & 63);
+    const size_t off = (static_cast<size_t>(blk) * Hkv + kvh) * 16 * HD;
+    const uint4* kt = reinterpret_cast<const uint4*>(kc + off);
+    const uint4* vt = reinterpret_cast<const uint4*>(vc + off);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int idx = tid + 256 * p;
+      const uint4* src = idx < KU ? kt + idx : vt + (idx - KU);
+      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)&skv[buf][256 * p + 64 * wave], 16, 0, 0);
+    }
+  };
 
   uint4 qh[NF], ql[NF];
   {
@@ -369,84 +395,83 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
 #pragma unroll
   for (int e = 0; e < NE; ++e) O[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const E* kc = static_cast<const E*>(kcv);
-  const E* vc = static_cast<const E*>(vcv);
-  for (int i = lo; i < hi; ++i) {
-    const int k = i - lo;
-    if ((k & 63) == 0 && k != 0) ids = i + lane < hi ? btrow[i + lane] : 0;
-    Blk B;
-    B.load(kc, vc, static_cast<size_t>(__builtin_amdgcn_readlane(ids, k & 63)) * Hkv + kvh, lane);
-    f32x4_t S = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      S = P::mma(S, B.kf[f], qh[f]);
-      if constexpr (kBf16) S = P::mma(S, B.kf[f], ql[f]);
+  issue(0, 0);
+  for (int i = 0; i < nblk; ++i) {
+    const int cur = i & 1;
+    // The next block goes into the other buffer, which every wave finished
+    // reading before the previous block's closing barrier.
+    if (i + 1 < nblk) {
+      if (((i + 1) & 63) == 0) ids = i + 1 + lane < nblk ? btrow[i + 1 + lane] : 0;
+      issue(i + 1, cur ^ 1);
+      wait_vmem<PER>();  // this thread's loads of block i have landed
+    } else {
+      wait_vmem<0>();
     }
-    if (i * 16 + 15 > tile.pos0) {  // block reaches past the tile's first position: causal mask
-      const int valid = pc - (i * 16 + 4 * g) + 1;
+    lds_stage_barrier();  // every thread's loads of block i have landed
+    if (rw > 0 && i * 16 <= wave_last) {  // wave-uniform: the block has keys some column sees
+      Blk B;
+      u32x4_t kr[NF], vr[NV];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) S[r] = r < valid ? S[r] : -INFINITY;
-    }
-    if (i == nblk - 1) B.mask_v(max_pos - (i * 16 + 4 * g) + 1);
-    float mb2 = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
-    mb2 = fmaxf(mb2, __shfl_xor(mb2, 16));
-    mb2 = fmaxf(mb2, __shfl_xor(mb2, 32));
-    const float m_new = fmaxf(m_run, mb2);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float p[4];
+      for (int f = 0; f < NF; ++f) kr[f] = lds_read16(&skv[cur][f * 64 + lane]);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(S[r] - m_use);
-    l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-    if (k != 0 && __ballot(m_new != m_run) != 0) {
+      for (int v = 0; v < NV; ++v) vr[v] = lds_read16(&skv[cur][KU + v * 64 + lane]);
+      lds_reads_done();
 #pragma unroll
-      for (int e = 0; e < NE; ++e) {
-        O[e][0] *= alpha;
-        O[e][1] *= alpha;
-        O[e][2] *= alpha;
-        O[e][3] *= alpha;
+      for (int f = 0; f < NF; ++f) {
+        lds_value_ready(kr[f]);
+        B.kf[f] = __builtin_bit_cast(uint4, kr[f]);
       }
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        lds_value_ready(vr[v]);
+        B.vf[v] = __builtin_bit_cast(uint4, vr[v]);
+      }
+      f32x4_t S = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        S = P::mma(S, B.kf[f], qh[f]);
+        if constexpr (kBf16) S = P::mma(S, B.kf[f], ql[f]);
+      }
+      if (i * 16 + 15 > tile.pos0 + r0) {  // block reaches past the wave's first position: causal mask
+        const int valid = pc - (i * 16 + 4 * g) + 1;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S[r] = r < valid ? S[r] : -INFINITY;
+      }
+      if (i == nblk - 1) B.mask_v(max_pos - (i * 16 + 4 * g) + 1);
+      float mb2 = fmaxf(fmaxf(S[0], S[1]), fmaxf(S[2], S[3]));
+      mb2 = fmaxf(mb2, __shfl_xor(mb2, 16));
+      mb2 = fmaxf(mb2, __shfl_xor(mb2, 32));
+      const float m_new = fmaxf(m_run, mb2);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      float p[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(S[r] - m_use);
+      l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+      if (i != 0 && __ballot(m_new != m_run) != 0) {
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+          O[e][0] *= alpha;
+          O[e][1] *= alpha;
+          O[e][2] *= alpha;
+          O[e][3] *= alpha;
+        }
+      }
+      m_run = m_new;
+      B.pv(O, p);
     }
-    m_run = m_new;
-    B.pv(O, p);
+    lds_stage_barrier();  // buffer cur is free for block i + 2
   }
+  if (rw <= 0) return;
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
-
-  __shared__ f32x4_t so[4][NE][64];
-  __shared__ float2 sml[4][64];
-  sml[wave][lane] = make_float2(m_run, l_run);
-#pragma unroll
-  for (int e = 0; e < NE; ++e) so[wave][e][lane] = O[e];
-  __syncthreads();
-  float2 ml[4];
-  float M = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    ml[w] = sml[w][lane];
-    M = fmaxf(M, ml[w].x);
-  }
-  float cw[4], L = 0.f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    cw[w] = __builtin_amdgcn_exp2f(ml[w].x - M);
-    L += cw[w] * ml[w].y;
-  }
-  if (c >= tile.n) return;
-  const float inv = 1.f / L;
+  if (c >= rw) return;
+  const float inv = 1.f / l_run;
   typename AP::elem* act = static_cast<typename AP::elem*>(actv);
 #pragma unroll
-  for (int k = 0; k < EPW; ++k) {
-    f32x4_t R = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const f32x4_t o = so[w][wave * EPW + k][lane];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) R[r] += cw[w] * o[r];
-    }
-    store_act4<AP>(act, Rp, tile.row0 + c, hq * HD + 16 * (wave * EPW + k) + 4 * g, R[0] * inv, R[1] * inv,
-                   R[2] * inv, R[3] * inv);
-  }
+  for (int e = 0; e < NE; ++e)
+    store_act4<AP>(act, Rp, tile.row0 + r0 + c, hq * HD + 16 * e + 4 * g, O[e][0] * inv, O[e][1] * inv,
+                   O[e][2] * inv, O[e][3] * inv);
 }
 
 // Rows src[k] of the residual as rows k of an activation record (Rp rows),

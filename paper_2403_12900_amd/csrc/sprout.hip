@@ -762,11 +762,11 @@ spr_status prefill_device(spr_model* m, int n, const int32_t* slots, const int32
       if (static_cast<int>(chunk_rows.size()) == spr::kPrefillRows) {
         if ((st = flush()) != SPR_OK) return st;
       }
-      // The next segment of request i that fits this chunk, in query tiles of 16.
+      // The next segment of request i that fits this chunk, in query tiles of 64.
       const int seg = std::min(seq_lens[i] - pos, spr::kPrefillRows - static_cast<int>(chunk_rows.size()));
       const int row0 = static_cast<int>(chunk_rows.size());
       for (int k = 0; k < seg; ++k) chunk_rows.push_back(PrefillRow{slots[i], pos + k, prompts[i][pos + k], 0});
-      for (int k = 0; k < seg; k += 16) tiles.push_back(PrefillTile{slots[i], row0 + k, std::min(16, seg - k), pos + k});
+      for (int k = 0; k < seg; k += 64) tiles.push_back(PrefillTile{slots[i], row0 + k, std::min(64, seg - k), pos + k});
       pos += seg;
       if (pos == seq_lens[i]) {
         ch.emit_row[ch.n_emit] = row0 + seg - 1;
