@@ -134,7 +134,23 @@ __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__
   __shared__ uint4 st2[NFRAG][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nt0 = blockIdx.x * TN, m0 = blockIdx.y * TM * 16;
+  // Work-groups go to the eight XCDs in turn (linear id mod 8), and each XCD
+  // has its own L2.  XCD x takes the contiguous range of tiles from x * total
+  // / 8 in an order that runs over groups of four row tiles, the row tile
+  // fastest: the 32 work-groups an XCD holds at a time then cover 8 weight
+  // tiles x 4 row tiles and fetch about 256 KB of operands per K-block instead
+  // of up to 1.5 MB.
+  int nt0, m0;
+  {
+    const int total = gridDim.x * gridDim.y, b = blockIdx.y * gridDim.x + blockIdx.x;
+    const int q = total / 8, r = total % 8, x = b % 8, j = b / 8;
+    const int t = x * q + min(x, r) + j;
+    const int gm = gridDim.y % 4 == 0 ? 4 : 1;
+    const int per_group = gm * gridDim.x;
+    const int mg = t / per_group, rem = t % per_group;
+    nt0 = (rem / gm) * TN;
+    m0 = (mg * gm + rem % gm) * TM * 16;
+  }
   const int wn = wave % TS::GN, wm = wave / TS::GN;
   const size_t xpart = static_cast<size_t>(Rp) * 4;  // uint4 per (K-block, part)
   const int xlane = (lane & 15) * 4 + (lane >> 4);   // uint4 of an activation fragment MFMA lane `lane` needs
