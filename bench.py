@@ -233,7 +233,7 @@ kernel_source_hash = {kernel_source_hash()}
 
 
 def time_prefill(model, m, wl, stops, reps: int = 3):
-    """Prefill of the whole batch (every prompt, chunks of up to 1024 rows),
+    """Prefill of the whole batch (every prompt, chunks of up to 4096 rows),
     re-run on freed slots.  Algorithmic flops: 2 x weight elements of the layer
     stack per prompt token, 4 x hd x H x (positions attended) per token and layer
     for attention, and the LM head for each prompt's last row; bf16 models issue

@@ -2,10 +2,11 @@
 // of up to kPrefillRows token rows, filling the KV cache (Section II-A: the
 // prompt's keys and values are computed once and cached; generation follows).
 // Unlike decode, each weight byte now meets hundreds of rows, so the
-// projections are compute-bound: a tiled MFMA GEMM stages 128 x 128 output
-// tiles through LDS.  Attention is causal over each request's own positions;
-// a wave's 16 MFMA columns are 16 consecutive query positions of one request
-// and head, so every K/V tile read feeds 16 queries.
+// projections are compute-bound: a tiled MFMA GEMM stages output tiles of up
+// to 256 x 256 through LDS.  Attention is causal over each request's own
+// positions; a wave's 16 MFMA columns are 16 consecutive query positions of
+// one request and head, and the four waves of a work-group share each K/V
+// tile they read from LDS, so every tile read feeds up to 64 queries.
 #pragma once
 
 #include "attn_kernels.h"
