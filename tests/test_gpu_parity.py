@@ -123,6 +123,16 @@ TOY_CASES = {
     "bf16_prompts_across_chunks": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
         [3000, 7, 2500, 40, 1800], [3, 4, 2, 5, 3]),
+    # The first chunk (4096 rows) ends exactly at the 96-row prompt's last row; the next chunk
+    # starts with a prompt at position 0.
+    "bf16_chunk_ends_at_prompt_end": (
+        ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
+        [4000, 96, 300, 5], [2, 3, 4, 2]),
+    # One prompt longer than a chunk: its first 4096 rows fill a chunk and its last 404 rows, with
+    # the next prompt, attend to them from the second.
+    "bf16_prompt_longer_than_a_chunk": (
+        ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=400),
+        [4500, 12], [3, 2]),
 }
 
 
