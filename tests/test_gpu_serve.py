@@ -75,6 +75,27 @@ def test_serve_matches_oracle(case):
     dm.close()
 
 
+def test_serve_empty_request_list_then_serves():
+    """No requests: success, zero counters, no KV block taken; the model then serves normally."""
+    from paper_2403_12900_amd.binding import DecodeModel
+    m, tol = CASES["bf16_gqa2"]
+    say("serve: empty request list, then 3 requests")
+    dm = DecodeModel(m, 91, max_slots=3, max_ctx=64, kv_blocks=12)
+    free0 = dm.free_blocks()
+    toks, st = dm.serve([], [], max_active=3)
+    assert toks == []
+    assert (st["iterations"], st["decode_steps"], st["prefill_calls"], st["decode_tokens"]) == (0, 0, 0, 0)
+    assert dm.free_blocks() == free0
+    rng = np.random.default_rng(5)
+    prompts = [rng.integers(0, m.vocab, size=n).astype(np.int32) for n in (9, 30, 17)]
+    stops = [6, 3, 8]
+    toks, st = dm.serve(prompts, stops, max_active=3)
+    assert [len(t) for t in toks] == stops and dm.free_blocks() == free0
+    ties, steps = check_tokens_against_oracle(R.Weights(oracle_shape(m), 91), prompts, toks, tol)
+    assert ties <= 1, (ties, steps)
+    dm.close()
+
+
 def test_serve_equals_closed_batch_7b():
     """Llama-2-7B shape: serving 24 requests 8 at a time gives the tokens of one closed batch, up to near-ties."""
     cfg = CONFIGS["c3"]

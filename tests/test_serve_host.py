@@ -100,6 +100,18 @@ def test_no_contention_matches_the_closed_batch_schedule():
     s.close()
 
 
+def test_empty_request_list_is_a_no_op():
+    """No requests: success, no prefill or decode call, and every KV block still free."""
+    s = Sched(max_slots=4, kv_blocks=64)
+    free0 = s.L.sprh_free_blocks(s.h)
+    st, per, batch, c = s.run([], [])
+    assert st == 0, s.L.sprh_last_error()
+    assert per == [] and batch == []
+    assert c == {"iterations": 0, "decode_steps": 0, "prefill_calls": 0, "decode_tokens": 0, "max_batch": 0}
+    assert s.L.sprh_free_blocks(s.h) == free0
+    s.close()
+
+
 def test_refills_retired_slots_in_order():
     rng = np.random.default_rng(7)
     stop = rng.integers(1, 30, size=40).tolist()
