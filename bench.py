@@ -132,6 +132,105 @@ def prefill_probe():
     model.close()
 
 
+def decode_probe():
+    """The c3 prefill, then one ragged decode of the batch (no timing), for a rocprofv3 --kernel-trace
+    that --trace-summary breaks down by active rows."""
+    import torch
+    from paper_2403_12900_amd.binding import DecodeModel
+    from paper_2403_12900_amd.configs import CONFIGS
+    from paper_2403_12900_amd.workload import make_workload
+    cfg = CONFIGS["c3"]
+    wl = make_workload(cfg)
+    seq = [int(x) for x in wl.seq_lens]
+    stops = [int(x) for x in wl.stop_lens]
+    max_ctx = max(s + L - 1 for s, L in zip(seq, stops))
+    blocks = sum((s + L - 1 + 15) // 16 for s, L in zip(seq, stops))
+    model = DecodeModel(cfg.model, cfg.weight_seed, max_slots=wl.batch, max_ctx=max_ctx, kv_blocks=blocks)
+    tok = model.new_token_buffer()
+    model.prefill(list(range(wl.batch)), wl.tokens, stops, tok)
+    for act, lens in _decode_schedule(seq, stops):
+        model.decode_step(act, lens, tok)
+    torch.cuda.synchronize()
+    log(f"decode probe: {len(_decode_schedule(seq, stops))} decode steps after the prefill")
+    model.close()
+
+
+def _decode_schedule(seq, stops):
+    """(active requests, their cached lengths) of every decode step of a closed ragged batch."""
+    return [([i for i in range(len(seq)) if stops[i] > s], [seq[i] + s - 1 for i in range(len(seq)) if stops[i] > s])
+            for s in range(1, max(stops))]
+
+
+def trace_summary(trace_dir: str) -> None:
+    """Prints the c3 decode's kernel time by active rows from the kernel_trace.csv that rocprofv3
+    wrote under trace_dir for `bench.py --decode-probe`.  Steps are split at each embedding launch;
+    per launch, the algorithmic bytes are the weights (projections) or the KV read of every active
+    row's cached positions and the new one (attention)."""
+    import csv
+    import glob
+    import re
+    from paper_2403_12900_amd.configs import CONFIGS
+    from paper_2403_12900_amd.workload import make_workload
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if len(paths) != 1:
+        raise SystemExit(f"{trace_dir}: expected one kernel_trace.csv, found {len(paths)}")
+    cfg = CONFIGS["c3"]
+    m = cfg.model
+    wl = make_workload(cfg)
+    sched = _decode_schedule([int(x) for x in wl.seq_lens], [int(x) for x in wl.stop_lens])
+    rows = []
+    with open(paths[0]) as fh:
+        for r in csv.DictReader(fh):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    starts = [i for i, r in enumerate(rows) if re.search(r"\bk_embed<", r[2])]
+    if len(starts) < len(sched):
+        raise SystemExit(f"{len(starts)} embedding launches for {len(sched)} decode steps")
+    starts = starts[-len(sched):] + [len(rows)]
+    d, hd, f, wb = m.d_model, m.head_dim, m.d_ff, m.weight_bytes
+    wbytes = {"QKV": m.qkv_rows * d * wb, "O": d * m.n_heads * hd * wb, "gate/up": 2 * f * d * wb, "down": d * f * wb}
+    kv_layer = m.kv_bytes_per_token() // m.n_layers
+    roles = ["QKV", "attention", "O", "gate/up", "down"]
+    bins = [("1", 1, 1), ("2-8", 2, 8), ("9-16", 9, 16), ("17-32", 17, 32)]
+    acc = {b[0]: {"steps": 0, "wall": 0.0, "kv": 0, **{r: 0.0 for r in roles}, "launches": 0} for b in bins}
+    for k, (act, lens) in enumerate(sched):
+        n = len(act)
+        a = next(acc[name] for name, lo, hi in bins if lo <= n <= hi)
+        step = rows[starts[k]:starts[k + 1]]
+        a["steps"] += 1
+        a["wall"] += (step[-1][1] - step[0][0]) / 1e3
+        a["kv"] += (sum(lens) + n) * kv_layer
+        resid = 0
+        for s0, s1, name in step:
+            us = (s1 - s0) / 1e3
+            if "EpiQKV" in name:
+                a["QKV"] += us
+                a["launches"] += 1
+            elif "k_attn_decode" in name:
+                a["attention"] += us
+            elif "EpiSwiGLU" in name:
+                a["gate/up"] += us
+            elif "EpiResid" in name:
+                a["O" if resid % 2 == 0 else "down"] += us
+                resid += 1
+    total = sum(a["wall"] for a in acc.values())
+    print("| active rows | steps | wall ms | " + " | ".join(roles) + " |")
+    print("|---|---:|---:|" + "---|" * len(roles))
+    for name, _, _ in bins:
+        a = acc[name]
+        if a["steps"] == 0:
+            continue
+        L = a["launches"]
+        cells = []
+        for r in roles:
+            us = a[r] / L
+            byts = a["kv"] / a["steps"] if r == "attention" else wbytes[r]
+            cells.append(f"{us:.1f} us, {byts / us / 1e3:.0f} GB/s")
+        print(f"| {name} | {a['steps']} | {a['wall'] / 1e3:.1f} | " + " | ".join(cells) + " |")
+    print(f"\nAll steps: {total / 1e3:.1f} ms from each step's first launch start to its last launch end; "
+          f"per launch: mean kernel time and algorithmic GB/s.")
+
+
 def step_sweep(key: str, steps: int = 12):
     """Decode-step time and algorithmic GB/s of one configuration's model at 1, 8, 16 and 32 rows of
     about 512 cached positions: the weights of every layer and the LM head, plus each row's KV read
@@ -399,6 +498,10 @@ def main():
                     help="decode-step GB/s of one configuration's model (c2..c5) at 1-32 rows of ~512 positions")
     ap.add_argument("--prefill-probe", action="store_true",
                     help="only run the c3 prefill twice (for rocprofv3 --pmc of the prefill GEMMs)")
+    ap.add_argument("--decode-probe", action="store_true",
+                    help="only run the c3 prefill and one ragged decode (for rocprofv3 --kernel-trace)")
+    ap.add_argument("--trace-summary", metavar="TRACE_DIR", default=None,
+                    help="print the decode's kernel time by active rows from a --decode-probe kernel trace")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only launch the dominant kernel and a calibration copy (for rocprofv3 --pmc)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -415,6 +518,12 @@ def main():
         return
     if args.prefill_probe:
         prefill_probe()
+        return
+    if args.decode_probe:
+        decode_probe()
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
         return
     if args.step_sweep:
         step_sweep(args.step_sweep)
