@@ -192,13 +192,15 @@ def trace_summary(trace_dir: str) -> None:
     kv_layer = m.kv_bytes_per_token() // m.n_layers
     roles = ["QKV", "attention", "O", "gate/up", "down"]
     bins = [("1", 1, 1), ("2-8", 2, 8), ("9-16", 9, 16), ("17-32", 17, 32)]
-    acc = {b[0]: {"steps": 0, "wall": 0.0, "kv": 0, **{r: 0.0 for r in roles}, "launches": 0} for b in bins}
+    acc = {b[0]: {"steps": 0, "wall": 0.0, "busy": 0.0, "kv": 0, **{r: 0.0 for r in roles}, "launches": 0}
+           for b in bins}
     for k, (act, lens) in enumerate(sched):
         n = len(act)
         a = next(acc[name] for name, lo, hi in bins if lo <= n <= hi)
         step = rows[starts[k]:starts[k + 1]]
         a["steps"] += 1
         a["wall"] += (step[-1][1] - step[0][0]) / 1e3
+        a["busy"] += sum(s1 - s0 for s0, s1, _ in step) / 1e3
         a["kv"] += (sum(lens) + n) * kv_layer
         resid = 0
         for s0, s1, name in step:
@@ -214,6 +216,8 @@ def trace_summary(trace_dir: str) -> None:
                 a["O" if resid % 2 == 0 else "down"] += us
                 resid += 1
     total = sum(a["wall"] for a in acc.values())
+    busy = sum(a["busy"] for a in acc.values())
+    launches = len(rows) - starts[0]
     print("| active rows | steps | wall ms | " + " | ".join(roles) + " |")
     print("|---|---:|---:|" + "---|" * len(roles))
     for name, _, _ in bins:
@@ -227,8 +231,10 @@ def trace_summary(trace_dir: str) -> None:
             byts = a["kv"] / a["steps"] if r == "attention" else wbytes[r]
             cells.append(f"{us:.1f} us, {byts / us / 1e3:.0f} GB/s")
         print(f"| {name} | {a['steps']} | {a['wall'] / 1e3:.1f} | " + " | ".join(cells) + " |")
-    print(f"\nAll steps: {total / 1e3:.1f} ms from each step's first launch start to its last launch end; "
-          f"per launch: mean kernel time and algorithmic GB/s.")
+    print(f"\nAll steps: {total / 1e3:.1f} ms from each step's first launch start to its last launch end, "
+          f"{busy / 1e3:.1f} ms of it in kernels: {(total - busy) / 1e3:.1f} ms between the decode's "
+          f"{launches} launches ({(total - busy) / launches:.2f} us each). Per launch in the table: mean "
+          f"kernel time and algorithmic GB/s.")
 
 
 def step_sweep(key: str, steps: int = 12):
