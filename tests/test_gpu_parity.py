@@ -118,6 +118,11 @@ TOY_CASES = {
     "bf16_mha32_splits_fit_resident": (
         ModelConfig(n_layers=1, d_model=256, n_heads=32, n_kv_heads=32, head_dim=64, d_ff=128, vocab=300),
         [140 + (i % 5) for i in range(24)], [3] * 24),
+    # The slot limit: 64 requests, so the first decode pass has 64 rows (four row tiles); later
+    # passes shrink through two and one row tiles as requests retire.
+    "bf16_batch64_max_slots": (
+        ModelConfig(n_layers=1, d_model=128, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=176, vocab=300),
+        [(7 * i) % 50 + 1 for i in range(64)], [(i % 6) + 2 for i in range(64)]),
     # A prompt spanning prefill chunks: 7347 rows run as chunks of 4096 and 3251 rows, and the
     # 2500-row prompt crosses the boundary at its row 1089.
     "bf16_prompts_across_chunks": (
