@@ -582,6 +582,8 @@ def main():
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
+    # Each slot's last token ends its greedy chain: repeated decodes must leave the same ones.
+    tok_ref = tok.clone() if args.warmup > 0 else None
     # One event pair brackets all timed steps (the reported mean); events between steps give each
     # step's own time for the median.
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
@@ -592,6 +594,10 @@ def main():
         marks[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    checks = {"tokens_repeat_exactly": None if tok_ref is None else bool(torch.equal(tok, tok_ref)),
+              "all_retired_at_stop": all(model.slot_info(i)[1] == stops[i] for i in range(B))}
+    if not all(v is not False for v in checks.values()):
+        log(f"WARNING: decode checks failed: {checks}")
     ms = marks[0].elapsed_time(marks[-1]) / args.steps
     per_step = [marks[k].elapsed_time(marks[k + 1]) for k in range(args.steps)]
     ms_median = float(np.median(per_step))
@@ -628,6 +634,7 @@ def main():
         "ms_per_step": round(ms, 3),
         "ms_per_step_median": round(ms_median, 3),
         "ms_per_step_runs": [round(x, 1) for x in per_step],
+        "checks": checks,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
