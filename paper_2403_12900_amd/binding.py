@@ -63,6 +63,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2403_12900_amd.build` "
                           "or __graft_entry__.build()")
+    # torch carries its own HIP runtime.  The library must bind to that one (it is handed torch's
+    # streams and device memory): loaded first, it would bring in the system runtime beside
+    # torch's, and that second runtime finds no device once torch's holds it.
+    import torch  # noqa: F401
     L = ctypes.CDLL(path)
     vp = ctypes.c_void_p
     L.spr_workspace_bytes.restype = ctypes.c_size_t

@@ -34,6 +34,15 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_library_shares_torchs_hip_runtime():
+    """One HIP runtime in the process: the library binds to the one torch brings, whose streams and
+    device memory it is handed.  A second copy (the library loaded before torch) found no device."""
+    binding.load_library()
+    maps = open("/proc/self/maps").read().splitlines()
+    hip = {line.split()[-1] for line in maps if "libamdhip64" in line and "/" in line}
+    assert len(hip) == 1, hip
+
+
 def test_workspace_bytes_and_invalid_configs():
     cfg = binding.make_config(LLAMA2_7B, 32, 2048, 32 * 128)
     n = binding.workspace_bytes(cfg)
