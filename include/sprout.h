@@ -137,9 +137,11 @@ spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots,
 
 /*
  * Rolls a prefilled slot back to `len` cached positions with `produced`
- * tokens generated (1 <= produced, len - produced + 1 >= 1 prompt position,
- * len <= current length).  Positions >= len are dropped; the slot is active
- * again if produced < its stop length.  Used to regenerate from a prompt.
+ * tokens generated.  The prompt stays: 1 <= produced <= the tokens produced
+ * so far, and len == prompt length + produced - 1 (SPR_ERR_INVALID_ARG
+ * otherwise; SPR_ERR_STATE for a free slot).  Positions >= len are dropped;
+ * the slot is active again if produced < its stop length.  Used to
+ * regenerate from a prompt.
  */
 spr_status spr_rewind_slot(spr_model* m, int32_t slot, int32_t len, int32_t produced);
 
