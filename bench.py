@@ -496,8 +496,6 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-serving", action="store_true", help="skip the continuous-batching measurement")
-    ap.add_argument("--decode-mode", type=int, default=None,
-                    help="0: one launch per kernel; 1: one persistent launch per layer (default: the library's)")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 32 gate/up and 32 O projections at 8 rows and 2 read-ceiling passes, for rocprofv3 --pmc")
     ap.add_argument("--step-sweep", metavar="CONFIG", default=None,
@@ -557,8 +555,6 @@ def main():
     torch.cuda.set_device(0)
     t0 = time.perf_counter()
     model = DecodeModel(m, cfg.weight_seed, max_slots=B, max_ctx=max_ctx, kv_blocks=blocks)
-    if args.decode_mode is not None:
-        model.set_decode_mode(args.decode_mode)
     tok = model.new_token_buffer()
     model.prefill(list(range(B)), wl.tokens, stops, tok)
     tok0 = tok.clone()

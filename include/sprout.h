@@ -20,6 +20,13 @@
  *     enqueued; a call that fails validation changes no state.
  *   - A HIP runtime failure (SPR_ERR_HIP) is sticky: every later call on that
  *     model returns SPR_ERR_HIP; the model must be released.
+ *   - Device-side checks: a decode step fed a token id outside [0, vocab)
+ *     (possible only through the caller-written device token buffer), or a
+ *     logits row holding a NaN or no finite maximum, sets a flag in mapped
+ *     host memory.  The first call that starts after the faulty work has
+ *     completed on the device returns SPR_ERR_DEVICE_CHECK, and so does every
+ *     later call: the model must be released.  (The step itself reads the
+ *     clamped id, or emits token 0, so no access leaves its buffers.)
  *   - Pointers marked "host" are read (or written) during the call only.
  *     Pointers marked "device" must stay valid until the work enqueued on the
  *     model's stream has completed; device outputs are valid once the caller
@@ -43,7 +50,8 @@ typedef enum {
   SPR_ERR_WORKSPACE = -2,   /* workspace missing, misaligned or too small */
   SPR_ERR_KV_FULL = -3,     /* not enough free KV-cache blocks */
   SPR_ERR_STATE = -4,       /* call does not match the slot state */
-  SPR_ERR_HIP = -5          /* HIP runtime error (sticky) */
+  SPR_ERR_HIP = -5,         /* HIP runtime error (sticky) */
+  SPR_ERR_DEVICE_CHECK = -6 /* a device-side check of an earlier call failed (sticky) */
 } spr_status;
 
 typedef enum { SPR_F32 = 0, SPR_BF16 = 1 } spr_dtype;
@@ -181,35 +189,15 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
 spr_status spr_time_projection(spr_model* m, int32_t projection, int32_t n_rows, int32_t reps, float* avg_us);
 
 /*
- * How a decode pass (spr_decode_step, and the decode steps of spr_serve) runs
- * the layer stack (Section II-A's per-token forward pass; the choice changes
- * launches, not results beyond floating-point summation order):
- *   0  one launch per kernel: QKV projection, attention, O, gate/up, down
- *      (the default);
- *   1  one persistent launch per layer for passes of at most 32 rows: the
- *      five phases run on a grid of resident work-groups (CUs x up to 3)
- *      separated by grid barriers; larger passes use mode 0.  If a grid
- *      barrier does not complete (a work-group that is never scheduled), the
- *      launch still ends and the next call on the model fails with
- *      SPR_ERR_HIP.
- * SPR_ERR_INVALID_ARG for another mode, or for 1 when the persistent launch
- * cannot keep its grid resident on this device.  Takes effect from the next
- * pass.
+ * Test aid (for tests of the greedy tie rule and of the device checks; no
+ * other caller needs it): overwrites row dst of the LM-head matrix, with row
+ * src when src >= 0 (a planted exact tie: both rows then give bitwise equal
+ * logits), else with `fill` rounded to the weight format (a NaN fill makes
+ * every later logits row hold a NaN).  The model is changed for the rest of
+ * its life.  dst in [0, vocab), src < vocab, else SPR_ERR_INVALID_ARG.
+ * Synchronous.
  */
-spr_status spr_set_decode_mode(spr_model* m, int32_t mode);
-
-/*
- * Test aid for the failure path of decode mode 1 (for tests of failure
- * handling; no other caller needs it): sets how many times a grid barrier of
- * a persistent layer launch polls before giving up (spin_limit, 64..2^20;
- * the default is 2^20, about a second), and adds skew to the barrier
- * generation the next persistent launch waits for.  With skew > 0 that
- * launch's barriers cannot complete: each wait gives up after spin_limit
- * polls, the launch still runs to its end (its outputs are meaningless), and
- * the next call on the model fails with SPR_ERR_HIP.  The model is then
- * unusable; release it.  SPR_ERR_INVALID_ARG for values out of range.
- */
-spr_status spr_test_barrier_timeout(spr_model* m, int32_t spin_limit, int32_t skew);
+spr_status spr_test_write_lm_head_row(spr_model* m, int32_t dst, int32_t src, float fill);
 
 /*
  * Measurement aid: the HBM read ceiling of the projections' load form.

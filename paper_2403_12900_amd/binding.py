@@ -18,6 +18,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libsprout.so")
 
 SPR_OK, SPR_ERR_INVALID_ARG, SPR_ERR_WORKSPACE, SPR_ERR_KV_FULL, SPR_ERR_STATE, SPR_ERR_HIP = 0, -1, -2, -3, -4, -5
+SPR_ERR_DEVICE_CHECK = -6
 SPR_F32, SPR_BF16 = 0, 1
 KV_BLOCK = 16
 TENSOR_IDS = {"embed": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "w1": 5, "w3": 6, "w2": 7, "lm_head": 8}
@@ -90,10 +91,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_time_projection.restype = ctypes.c_int
     L.spr_time_projection.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_float)]
-    L.spr_set_decode_mode.restype = ctypes.c_int
-    L.spr_set_decode_mode.argtypes = [vp, ctypes.c_int32]
-    L.spr_test_barrier_timeout.restype = ctypes.c_int
-    L.spr_test_barrier_timeout.argtypes = [vp, ctypes.c_int32, ctypes.c_int32]
+    L.spr_test_write_lm_head_row.restype = ctypes.c_int
+    L.spr_test_write_lm_head_row.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_float]
     L.spr_time_read_ceiling.restype = ctypes.c_int
     L.spr_time_read_ceiling.argtypes = [vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_uint64)]
@@ -212,13 +211,9 @@ class DecodeModel:
         _check(self.lib.spr_time_projection(self.h, self.PROJECTIONS[projection], n_rows, reps, ctypes.byref(out)))
         return float(out.value)
 
-    def set_decode_mode(self, mode: int):
-        """0: one launch per kernel; 1: one persistent launch per layer for passes of at most 32 rows."""
-        _check(self.lib.spr_set_decode_mode(self.h, mode))
-
-    def test_barrier_timeout(self, spin_limit: int, skew: int):
-        """Failure-path test aid of decode mode 1 (see spr_test_barrier_timeout)."""
-        _check(self.lib.spr_test_barrier_timeout(self.h, spin_limit, skew))
+    def test_write_lm_head_row(self, dst: int, src: int = -1, fill: float = 0.0):
+        """Test aid: LM-head row dst := row src (src >= 0) or the constant fill (see spr_test_write_lm_head_row)."""
+        _check(self.lib.spr_test_write_lm_head_row(self.h, dst, src, fill))
 
     def read_ceiling(self, reps: int = 5):
         """(GB/s, bytes per pass): plain streaming read of every weight matrix, timed on the model's stream."""

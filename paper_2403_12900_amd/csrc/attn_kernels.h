@@ -56,7 +56,7 @@ __device__ __forceinline__ float2 load_coherent2(const float* p) {
 // row's split count within one round.
 constexpr int kMergeChunk = 16;
 
-template <class AP, int HD, bool kCoh>
+template <class AP, int HD>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns);
 
 // K and V of one 16-position block of one KV head, in registers: NF K
@@ -158,10 +158,8 @@ struct AttnSmem {
 };
 
 // The body of k_attn_decode for work item (flat split f, KV head kvh), run by
-// all four waves of the calling work-group.  kCoh: the output activation is
-// read by other work-groups of the same launch (the persistent layer kernel),
-// so it goes out as agent-coherent stores.
-template <class P, class AP, int HD, bool kCoh>
+// all four waves of the calling work-group.
+template <class P, class AP, int HD>
 __device__ __forceinline__ void attn_decode_unit(const AttnArgs& a, int f, int kvh, AttnSmem<HD>* sm) {
   using E = typename P::elem;
   using Blk = KVBlock<P, HD>;
@@ -313,8 +311,7 @@ __device__ __forceinline__ void attn_decode_unit(const AttnArgs& a, int f, int k
 #pragma unroll
     for (int k = 0; k < EPW; ++k) {
       const int n0 = hq * HD + 16 * (wave * EPW + k) + 4 * g;
-      if constexpr (kCoh) act_store4_coh<AP>(act, a.Rp, b, n0, R[k][0] * inv, R[k][1] * inv, R[k][2] * inv, R[k][3] * inv);
-      else store_act4<AP>(act, a.Rp, b, n0, R[k][0] * inv, R[k][1] * inv, R[k][2] * inv, R[k][3] * inv);
+      store_act4<AP>(act, a.Rp, b, n0, R[k][0] * inv, R[k][1] * inv, R[k][2] * inv, R[k][3] * inv);
     }
     return;
   }
@@ -341,20 +338,20 @@ __device__ __forceinline__ void attn_decode_unit(const AttnArgs& a, int f, int k
   __syncthreads();
   if (!sm->last) return;
   if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  merge_splits<AP, HD, kCoh>(a, b, kvh, a.split_start[b], nsplit);
+  merge_splits<AP, HD>(a, b, kvh, a.split_start[b], nsplit);
 }
 
 template <class P, class AP, int HD>
 __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   __shared__ AttnSmem<HD> sm;
-  attn_decode_unit<P, AP, HD, false>(a, blockIdx.x, blockIdx.y, &sm);
+  attn_decode_unit<P, AP, HD>(a, blockIdx.x, blockIdx.y, &sm);
 }
 
 // Log-sum-exp merge of the nsplit partials of one (row, KV head), run by the
 // split that arrived last.  Splits are taken kChunk at a time, all of a
 // chunk's loads issued before any is combined (indexes past the last split
 // re-read it and are then ignored).
-template <class AP, int HD, bool kCoh>
+template <class AP, int HD>
 __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, int f0, int ns) {
   constexpr int kChunk = kMergeChunk;
   typename AP::elem* act = static_cast<typename AP::elem*>(a.act);
@@ -387,8 +384,7 @@ __device__ __forceinline__ void merge_splits(const AttnArgs& a, int b, int kvh, 
       }
       M = Mn;
     }
-    if constexpr (kCoh) act_store_coh<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
-    else act_store<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
+    act_store<AP>(act, a.Rp, b, hq * HD + dd, Ov / L);
   }
 }
 

@@ -136,95 +136,6 @@ __device__ __forceinline__ void act_store(typename P::elem* act, int Rp, int b, 
 }
 
 // ---------------------------------------------------------------------------
-// Agent-coherent stores and loads: relaxed device-scope atomics, which gfx950
-// issues as global_store / global_load with the sc1 bit.  A work-group that
-// hands data to another work-group of the same launch, on any XCD, stores it
-// this way and drains its vmcnt before signalling; the reader loads it the
-// same way (or, if it has never read those bytes in this launch, plainly).
-// No write-back of an XCD's L2 is involved.
-__device__ __forceinline__ void st_coh(uint16_t* p, uint16_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_coh(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_coh(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_coh(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t pack2(float a, float b) {
-  return static_cast<uint64_t>(__float_as_uint(a)) | (static_cast<uint64_t>(__float_as_uint(b)) << 32);
-}
-__device__ __forceinline__ uint64_t pack4(uint16_t a, uint16_t b, uint16_t c, uint16_t d) {
-  return static_cast<uint64_t>(a) | (static_cast<uint64_t>(b) << 16) | (static_cast<uint64_t>(c) << 32) |
-         (static_cast<uint64_t>(d) << 48);
-}
-// Four consecutive fp32 values (16-byte aligned) and their coherent load.
-__device__ __forceinline__ void st_coh_f4(float* p, float a, float b, float c, float d) {
-  st_coh(reinterpret_cast<uint64_t*>(p), pack2(a, b));
-  st_coh(reinterpret_cast<uint64_t*>(p) + 1, pack2(c, d));
-}
-__device__ __forceinline__ float4 ld_coh_f4(const float* p) {
-  const uint64_t u = ld_coh(reinterpret_cast<const uint64_t*>(p)), v = ld_coh(reinterpret_cast<const uint64_t*>(p) + 1);
-  return make_float4(__uint_as_float(static_cast<uint32_t>(u)), __uint_as_float(static_cast<uint32_t>(u >> 32)),
-                     __uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
-}
-// One element of a storage format, coherently.
-__device__ __forceinline__ void st_coh_elem(uint16_t* p, uint16_t v) { st_coh(p, v); }
-__device__ __forceinline__ void st_coh_elem(float* p, float v) { st_coh(reinterpret_cast<uint32_t*>(p), __float_as_uint(v)); }
-// Four consecutive elements of a storage format (8-byte aligned for bf16, 16 for fp32), coherently.
-template <class P>
-__device__ __forceinline__ void st_coh_elem4(typename P::elem* p, float a, float b, float c, float d) {
-  if constexpr (sizeof(typename P::elem) == 2) {
-    st_coh(reinterpret_cast<uint64_t*>(p), pack4(P::from_f32(a), P::from_f32(b), P::from_f32(c), P::from_f32(d)));
-  } else {
-    st_coh_f4(reinterpret_cast<float*>(p), a, b, c, d);
-  }
-}
-
-// Activation record stores, coherently: one value, two consecutive features
-// (an even first feature) or four (a first feature divisible by four); the
-// features of one row and part within a K-block are contiguous.
-template <class P>
-__device__ __forceinline__ void act_store_coh(typename P::elem* act, int Rp, int b, int k, float v) {
-  typename P::elem hi, lo;
-  P::split(v, &hi, &lo);
-  st_coh_elem(act + act_offset<P>(Rp, b, k, 0), hi);
-  if constexpr (P::parts == 2) st_coh_elem(act + act_offset<P>(Rp, b, k, 1), lo);
-}
-template <class P>
-__device__ __forceinline__ void act_store2_coh(typename P::elem* act, int Rp, int b, int k, float v0, float v1) {
-  typename P::elem h0, l0, h1, l1;
-  P::split(v0, &h0, &l0);
-  P::split(v1, &h1, &l1);
-  if constexpr (sizeof(typename P::elem) == 2) {
-    st_coh(reinterpret_cast<uint32_t*>(act + act_offset<P>(Rp, b, k, 0)), static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16));
-    if constexpr (P::parts == 2)
-      st_coh(reinterpret_cast<uint32_t*>(act + act_offset<P>(Rp, b, k, 1)), static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16));
-  } else {
-    st_coh(reinterpret_cast<uint64_t*>(act + act_offset<P>(Rp, b, k, 0)), pack2(h0, h1));
-  }
-}
-template <class P>
-__device__ __forceinline__ void act_store4_coh(typename P::elem* act, int Rp, int b, int k, float v0, float v1, float v2,
-                                               float v3) {
-  typename P::elem h[4], l[4];
-  P::split(v0, &h[0], &l[0]);
-  P::split(v1, &h[1], &l[1]);
-  P::split(v2, &h[2], &l[2]);
-  P::split(v3, &h[3], &l[3]);
-  if constexpr (sizeof(typename P::elem) == 2) {
-    st_coh(reinterpret_cast<uint64_t*>(act + act_offset<P>(Rp, b, k, 0)), pack4(h[0], h[1], h[2], h[3]));
-    if constexpr (P::parts == 2)
-      st_coh(reinterpret_cast<uint64_t*>(act + act_offset<P>(Rp, b, k, 1)), pack4(l[0], l[1], l[2], l[3]));
-  } else {
-    st_coh_f4(reinterpret_cast<float*>(act + act_offset<P>(Rp, b, k, 0)), h[0], h[1], h[2], h[3]);
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Counter-based N(0, 0.02) weight draw.  SplitMix64 (Steele, Lea, Flood,
 // OOPSLA 2014): the n-th output of a stream seeded with s is
 // mix(s + n * 0x9E3779B97F4A7C15).  A matrix (tensor t, layer l) uses the

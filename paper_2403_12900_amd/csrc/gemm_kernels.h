@@ -94,41 +94,16 @@ struct StreamRed {
 template <class P, int JT, int RT, int U>
 using StreamStageOf = StreamStage<P, JT, RT, (U / 2 > 0 ? U / 2 : 1)>;
 
-// Issues the weight loads of the first two pipeline stages of a wave's
-// stream (as stream_gemm_tiles with the same arguments would), so they are in
-// flight before the activations they multiply exist; stream_gemm_tiles with
-// PF = 2 then issues only the activations of those stages.
-template <class P, int JT, int WAVES, int RT, int U, bool kStream>
-__device__ __forceinline__ void stream_prefetch_weights(const uint4* __restrict__ W, int KB, int nt0, int wave,
-                                                        int lane, StreamStageOf<P, JT, RT, U>& s0,
-                                                        StreamStageOf<P, JT, RT, U>& s1) {
-  constexpr int UH = U / 2 > 0 ? U / 2 : 1;
-  const int kb0 = (KB * wave) / WAVES, kb1 = (KB * (wave + 1)) / WAVES;
-  const int nstage = (kb1 - kb0) / UH;
-  const uint4* wp = W + static_cast<size_t>(nt0) * KB * 64 + lane;
-  const size_t wtile = static_cast<size_t>(KB) * 64;
-  auto load_w = [&](StreamStageOf<P, JT, RT, U>& st, int kb) {
-#pragma unroll
-    for (int u = 0; u < UH; ++u)
-#pragma unroll
-      for (int t = 0; t < RT; ++t) st.a[u][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb + u) * 64);
-  };
-  if (nstage > 0) load_w(s0, kb0);
-  if (nstage > 1) load_w(s1, kb0 + UH);
-}
-
 // The body of k_stream_gemm as a device function: the WAVES waves of the
 // calling work-group compute row tiles nt0 .. nt0 + RT - 1; red is LDS of
 // StreamRed<JT, WAVES, RT>::floats floats.  With WAVES > 1 every wave of the
 // work-group must call it (it synchronises the work-group).  s0, s1 are the
-// pipeline stages; PF = 2: stream_prefetch_weights has already issued their
-// weight loads.
-template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream, int PF = 0>
+// pipeline stages.
+template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream>
 __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, const uint4* __restrict__ X, int KB,
                                                   int Rp, int n_rows, const Epi& epi, int nt0, int wave, int lane,
                                                   float* red, StreamStageOf<P, JT, RT, U>& s0,
                                                   StreamStageOf<P, JT, RT, U>& s1) {
-  static_assert(PF == 0 || PF == 2, "prefetched stages: none or both");
   constexpr int PARTS = P::parts;
   constexpr int UH = U / 2 > 0 ? U / 2 : 1;
   using Stage = StreamStageOf<P, JT, RT, U>;
@@ -173,14 +148,6 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
         for (int q = 0; q < PARTS; ++q) st.x[u][j][q] = X[(static_cast<size_t>(kb + u) * PARTS + q) * xpart + xoff[j]];
     }
   };
-  auto load_x = [&](Stage& st, int kb) {
-#pragma unroll
-    for (int u = 0; u < UH; ++u)
-#pragma unroll
-      for (int j = 0; j < JT; ++j)
-#pragma unroll
-        for (int q = 0; q < PARTS; ++q) st.x[u][j][q] = X[(static_cast<size_t>(kb + u) * PARTS + q) * xpart + xoff[j]];
-  };
   auto compute = [&](const Stage& st) {
 #pragma unroll
     for (int u = 0; u < UH; ++u) {
@@ -199,14 +166,9 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
   };
 
   const int nstage = (kb1 - kb0) / UH;
-  if constexpr (PF == 2) {
-    if (nstage > 0) load_x(s0, kb0);
-    if (nstage > 1) load_x(s1, kb0 + UH);
-  } else {
-    if (nstage > 0) load(s0, kb0);
-  }
+  if (nstage > 0) load(s0, kb0);
   for (int c = 0; c < nstage; c += 2) {
-    if (c + 1 < nstage && (PF == 0 || c > 0)) load(s1, kb0 + (c + 1) * UH);
+    if (c + 1 < nstage) load(s1, kb0 + (c + 1) * UH);
     compute(s0);
     if (c + 1 < nstage) {
       if (c + 2 < nstage) load(s0, kb0 + (c + 2) * UH);
@@ -295,9 +257,7 @@ __device__ __forceinline__ void store_act4(typename P::elem* act, int Rp, int b,
 // order (ktile_offset) and the V tile is transposed into the operand order of
 // the P V product (vtile_offset), so the attention kernel reads both with
 // 16-byte loads straight into MFMA operands.
-// kCoh: the outputs are read by other work-groups of the same launch (the
-// persistent layer kernel), so they go out as agent-coherent stores.
-template <class P, class KP = P, bool kCoh = false>
+template <class P, class KP = P>
 struct EpiQKV {
   static constexpr bool kNorm = true;
   int n_rows, H, Hkv, hd, mb, dnorm;
@@ -356,8 +316,7 @@ struct EpiQKV {
         v3 = a3;
       }
       if (n0 < qr) {
-        if constexpr (kCoh) st_coh_f4(q + static_cast<size_t>(b) * qr + n0, v0, v1, v2, v3);
-        else *reinterpret_cast<float4*>(q + static_cast<size_t>(b) * qr + n0) = make_float4(v0, v1, v2, v3);
+        *reinterpret_cast<float4*>(q + static_cast<size_t>(b) * qr + n0) = make_float4(v0, v1, v2, v3);
         continue;
       }
       const int blk = pr.blk[j];
@@ -365,28 +324,17 @@ struct EpiQKV {
       if (n0 < qr + kr) {
         const int m = n0 - qr, kvh = m / hd, dd = m % hd;
         typename KP::elem* dst = kc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd + ktile_offset<KP>(off, dd);
-        if constexpr (kCoh) {
-          st_coh_elem4<KP>(dst, v0, v1, v2, v3);
-        } else {
-          dst[0] = KP::from_f32(v0);
-          dst[1] = KP::from_f32(v1);
-          dst[2] = KP::from_f32(v2);
-          dst[3] = KP::from_f32(v3);
-        }
+        dst[0] = KP::from_f32(v0);
+        dst[1] = KP::from_f32(v1);
+        dst[2] = KP::from_f32(v2);
+        dst[3] = KP::from_f32(v3);
       } else {
         const int m = n0 - qr - kr, kvh = m / hd, dd = m % hd;
         typename KP::elem* dst = vc + (static_cast<size_t>(blk) * Hkv + kvh) * 16 * hd;
-        if constexpr (kCoh) {
-          st_coh_elem(dst + vtile_offset<KP>(off, dd), KP::from_f32(v0));
-          st_coh_elem(dst + vtile_offset<KP>(off, dd + 1), KP::from_f32(v1));
-          st_coh_elem(dst + vtile_offset<KP>(off, dd + 2), KP::from_f32(v2));
-          st_coh_elem(dst + vtile_offset<KP>(off, dd + 3), KP::from_f32(v3));
-        } else {
-          dst[vtile_offset<KP>(off, dd)] = KP::from_f32(v0);
-          dst[vtile_offset<KP>(off, dd + 1)] = KP::from_f32(v1);
-          dst[vtile_offset<KP>(off, dd + 2)] = KP::from_f32(v2);
-          dst[vtile_offset<KP>(off, dd + 3)] = KP::from_f32(v3);
-        }
+        dst[vtile_offset<KP>(off, dd)] = KP::from_f32(v0);
+        dst[vtile_offset<KP>(off, dd + 1)] = KP::from_f32(v1);
+        dst[vtile_offset<KP>(off, dd + 2)] = KP::from_f32(v2);
+        dst[vtile_offset<KP>(off, dd + 3)] = KP::from_f32(v3);
       }
     }
   }
@@ -394,7 +342,7 @@ struct EpiQKV {
 
 // O and down projections: residual add, then the new residual in the
 // activation format for the next projection.
-template <class P, bool kCoh = false>
+template <class P>
 struct EpiResid {
   static constexpr bool kNorm = false;
   int n_rows, d, Rp;
@@ -414,8 +362,7 @@ struct EpiResid {
     for (int j = 0; j < JT; ++j) {
       const int b = 16 * j + (lane & 15);
       const float* xp = x + static_cast<size_t>(b < n_rows ? b : 0) * d + n0;
-      if constexpr (kCoh) pr.x[j] = ld_coh_f4(xp);
-      else pr.x[j] = *reinterpret_cast<const float4*>(xp);
+      pr.x[j] = *reinterpret_cast<const float4*>(xp);
     }
     return pr;
   }
@@ -433,20 +380,15 @@ struct EpiResid {
       xv.y += acc[j][1];
       xv.z += acc[j][2];
       xv.w += acc[j][3];
-      if constexpr (kCoh) {
-        st_coh_f4(reinterpret_cast<float*>(xp), xv.x, xv.y, xv.z, xv.w);
-        act_store4_coh<P>(act, Rp, b, n0, xv.x, xv.y, xv.z, xv.w);
-      } else {
-        *xp = xv;
-        store_act4<P>(act, Rp, b, n0, xv.x, xv.y, xv.z, xv.w);
-      }
+      *xp = xv;
+      store_act4<P>(act, Rp, b, n0, xv.x, xv.y, xv.z, xv.w);
     }
   }
 };
 
 // Gate/up projection (interleaved rows, see wgen_kernels.h): RMSNorm scale,
 // then h = SiLU(gate) * up for two features per lane.
-template <class P, bool kCoh = false>
+template <class P>
 struct EpiSwiGLU {
   static constexpr bool kNorm = true;
   int n_rows, dnorm, Rp;
@@ -470,12 +412,8 @@ struct EpiSwiGLU {
       const float g0 = acc[j][0] * s, g1 = acc[j][1] * s, u0 = acc[j][2] * s, u1 = acc[j][3] * s;
       const float h0 = g0 / (1.f + __expf(-g0)) * u0;
       const float h1 = g1 / (1.f + __expf(-g1)) * u1;
-      if constexpr (kCoh) {
-        act_store2_coh<P>(act, Rp, b, j0, h0, h1);
-      } else {
-        act_store<P>(act, Rp, b, j0, h0);
-        act_store<P>(act, Rp, b, j0 + 1, h1);
-      }
+      act_store<P>(act, Rp, b, j0, h0);
+      act_store<P>(act, Rp, b, j0 + 1, h1);
     }
   }
 };
@@ -507,6 +445,7 @@ struct EpiLogits {
       const float s = rsqrtf(ssq[j] / static_cast<float>(dnorm) + eps);
       float best = -INFINITY;
       int bi = 0x7fffffff;
+      int nan = 0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float z = acc[j][i] * s;
@@ -515,18 +454,22 @@ struct EpiLogits {
           best = z;
           bi = n;
         }
+        nan |= n < V && z != z;
         if (vb && logits != nullptr && n < V && out_row[b] >= 0) logits[static_cast<size_t>(out_row[b]) * V + n] = z;
       }
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
         const float ob = __shfl_xor(best, o);
         const int oi = __shfl_xor(bi, o);
+        nan |= __shfl_xor(nan, o);
         if (ob > best || (ob == best && oi < bi)) {
           best = ob;
           bi = oi;
         }
       }
-      if ((lane >> 4) == 0 && vb) part[static_cast<size_t>(nt) * kRows + b] = make_float2(best, __int_as_float(bi));
+      // A NaN logit makes the tile's candidate value NaN (k_argmax_final reports it).
+      if ((lane >> 4) == 0 && vb)
+        part[static_cast<size_t>(nt) * kRows + b] = make_float2(nan ? __int_as_float(0x7fc00000) : best, __int_as_float(bi));
     }
   }
 };

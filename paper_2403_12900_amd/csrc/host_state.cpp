@@ -113,12 +113,6 @@ Layout layout(const Dims& d) {
   // Split arrival counters of decode attention, one per (row, KV head); zero between launches.
   l.off_cnt = take(static_cast<size_t>(kMaxRows) * d.Hkv * sizeof(int32_t));
   l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
-  // The persistent layer launch reads each phase's activation record from its own buffer:
-  // two records more, sized for a decode pass.
-  l.dec_act_bytes = static_cast<size_t>(d.kb_max) * kMaxRows * d.kblk * d.esize * (d.dtype == SPR_BF16 ? 2 : 1);
-  l.off_act2 = take(l.dec_act_bytes);
-  l.off_act3 = take(l.dec_act_bytes);
-  l.off_bar = take(kBarBytes);
   l.off_prow = take(static_cast<size_t>(kPrefillRows) * 4 * sizeof(int32_t));
   l.off_ptile = take(static_cast<size_t>(kPrefillTiles) * 4 * sizeof(int32_t));
   l.off_rs = take(static_cast<size_t>(kPrefillRows) * sizeof(float));

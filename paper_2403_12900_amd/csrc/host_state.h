@@ -15,7 +15,6 @@
 namespace spr {
 
 constexpr int kKvBlock = 16;     // positions per KV block
-constexpr int kBarBytes = 4 * 64 * (2 * 32 + 1);  // grid barrier words of the persistent layer launch
 constexpr int kMaxRows = 128;    // token rows per decode pass (and LM-head rows of a prefill chunk)
 // Token rows per prefill chunk.  Chunks fill up in request order.  At 7B
 // shapes, 32 prompts of 8427 tokens in all ran 14% faster in 4096-row chunks
@@ -42,7 +41,6 @@ struct Layout {
   size_t off_wqkv, off_wo, off_w13, off_w2, off_wlm, off_emb;
   size_t off_rope, off_kc, off_vc, kv_layer_stride, off_bt;
   size_t off_x, off_act0, off_act1, act_bytes, off_q, off_part, off_cnt, off_amax;
-  size_t off_act2, off_act3, dec_act_bytes, off_bar;  // persistent layer launch: two more records, barrier words
   size_t off_prow, off_ptile, off_rs;  // prefill chunk: row table, query tiles, RMSNorm scales
   size_t total;
 };

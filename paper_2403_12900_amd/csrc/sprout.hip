@@ -27,7 +27,6 @@
 #include <vector>
 
 #include "attn_kernels.h"
-#include "layer_kernels.h"
 #include "gemm_kernels.h"
 #include "host_state.h"
 #include "prefill_kernels.h"
@@ -38,9 +37,6 @@ using namespace sprk;
 
 static_assert(spr::kPrefillRows == sprk::kPrefillRows, "prefill chunk size");
 static_assert(spr::kMaxRows == sprk::kRows, "decode pass size");
-static_assert(spr::kBarBytes == 4 * sprk::kBarWords, "grid barrier words");
-static_assert(sizeof(sprk::LayerArgs) + sizeof(sprk::LayerEpis<sprk::BF16, sprk::F32>) <= 4096,
-              "persistent layer launch arguments exceed the kernel argument segment");
 
 struct spr_model {
   spr::Dims d{};
@@ -49,18 +45,17 @@ struct spr_model {
   hipStream_t st = nullptr;
   spr::SlotTable tab;
   std::vector<int32_t> bt_row;
-  bool sticky = false;
+  // A failure that leaves the model unusable (a HIP error, or a failed device
+  // check of an earlier step): every later call returns it.
+  spr_status sticky = SPR_OK;
+  std::string sticky_msg;
   uint64_t seed = 0;
-  // Persistent layer launch (decode mode 1): grid size (0 = unavailable), the
-  // barrier generation the next launch starts from, and the timeout flag in
-  // mapped pinned host memory (host and device views).
-  int decode_mode = 0;
-  int layer_grid = 0;
   // Decode attention work-groups resident at once (CUs x occupancy).
   int attn_slots = 1024;
-  unsigned bar_gen = 0;
-  int bar_spin_limit = sprk::kBarSpinLimit;
-  unsigned bar_skew = 0;  // test aid: added to the next launch's barrier generations
+  // Device-side error flag in mapped pinned host memory (host and device
+  // views): kernels set a bit when a step met an input they cannot honour (a
+  // token id outside the vocabulary, a logits row with no finite maximum);
+  // the next call on the model reports it.
   int* err_host = nullptr;
   int* err_dev = nullptr;
   ~spr_model() {
@@ -78,8 +73,12 @@ spr_status fail(spr_status s, const std::string& msg) {
 }
 
 spr_status hip_fail(spr_model* m, const char* what, hipError_t e) {
-  if (m) m->sticky = true;
-  return fail(SPR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  const std::string msg = std::string(what) + ": " + hipGetErrorString(e);
+  if (m) {
+    m->sticky = SPR_ERR_HIP;
+    m->sticky_msg = "an earlier HIP error left the model unusable; release it (" + msg + ")";
+  }
+  return fail(SPR_ERR_HIP, msg);
 }
 
 #define SPR_HIP(m, expr)                               \
@@ -151,10 +150,7 @@ struct Ptrs {
   char* vc(int layer) const { return ws + l->off_vc + l->kv_layer_stride * layer; }
   int32_t* bt() const { return reinterpret_cast<int32_t*>(ws + l->off_bt); }
   float* x() const { return reinterpret_cast<float*>(ws + l->off_x); }
-  char* act(int i) const {
-    return ws + (i == 0 ? l->off_act0 : i == 1 ? l->off_act1 : i == 2 ? l->off_act2 : l->off_act3);
-  }
-  unsigned* bar() const { return reinterpret_cast<unsigned*>(ws + l->off_bar); }
+  char* act(int i) const { return ws + (i == 0 ? l->off_act0 : l->off_act1); }
   float* q() const { return reinterpret_cast<float*>(ws + l->off_q); }
   float* part() const { return reinterpret_cast<float*>(ws + l->off_part); }
   int32_t* cnt() const { return reinterpret_cast<int32_t*>(ws + l->off_cnt); }
@@ -251,10 +247,6 @@ spr_status launch_attention(spr_model* m, const AttnArgs& a) {
   return SPR_OK;
 }
 
-// Whether the persistent layer launch streams gate/up in one-wave two-tile
-// units (the per-kernel path's shape for projections this wide).
-inline bool wide_gate_up(const spr::Dims& d) { return d.nt_13 >= 1024 && d.nt_13 % 2 == 0; }
-
 // Attention arguments of one layer over rs (kv splits of bpw blocks per wave).
 template <class P, class KP>
 AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int Rp, int bpw, void* act) {
@@ -280,101 +272,6 @@ AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos&
   a.split_start[0] = 0;
   for (int r = 0; r < rs.n; ++r) a.split_start[r + 1] = a.split_start[r] + ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw);
   return a;
-}
-
-// One layer of a decode pass of at most 32 rows as a single persistent launch
-// (k_decode_layer): the phases read act(0), act(1), act(2), act(3) and the
-// down projection writes act(0) for the next layer.
-template <class P, class KP>
-spr_status launch_layer(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int JT, int bpw) {
-  const spr::Dims& d = m->d;
-  Ptrs p{m->ws, &m->lay};
-  using E = typename P::elem;
-  const int n = rs.n, Rp = 16 * JT;
-  if (m->bar_gen > (1u << 24)) {  // keep the accumulated counts far from overflow
-    SPR_HIP(m, hipMemsetAsync(p.bar(), 0, spr::kBarBytes, m->st));
-    m->bar_gen = 0;
-  }
-  LayerArgs a{};
-  a.wqkv = reinterpret_cast<const uint4*>(p.wqkv(l));
-  a.wo = reinterpret_cast<const uint4*>(p.wo(l));
-  a.w13 = reinterpret_cast<const uint4*>(p.w13(l));
-  a.w2 = reinterpret_cast<const uint4*>(p.w2(l));
-  a.act_in = reinterpret_cast<const uint4*>(p.act(0));
-  a.act_attn = reinterpret_cast<const uint4*>(p.act(1));
-  a.act_mid = reinterpret_cast<const uint4*>(p.act(2));
-  a.act_h = reinterpret_cast<const uint4*>(p.act(3));
-  a.n_rows = n;
-  a.Rp = Rp;
-  a.nt_qkv = d.nt_qkv;
-  a.nt_o = d.nt_o;
-  a.nt_13 = d.nt_13;
-  a.nt_2 = d.nt_2;
-  a.kb_d = d.kb_d;
-  a.kb_o = d.kb_o;
-  a.kb_f = d.kb_f;
-  a.attn = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1));
-  a.n_units = a.attn.split_start[n] * d.Hkv;
-  a.bar = p.bar();
-  a.gen0 = m->bar_gen + m->bar_skew;
-  a.spin_limit = m->bar_spin_limit;
-  a.err = m->err_dev;
-  m->bar_gen += 4;
-  m->bar_skew = 0;
-
-  LayerEpis<P, KP> e{};
-  e.qkv.n_rows = n;
-  e.qkv.H = d.H;
-  e.qkv.Hkv = d.Hkv;
-  e.qkv.hd = d.hd;
-  e.qkv.mb = d.mb;
-  e.qkv.dnorm = d.d;
-  e.qkv.eps = d.eps;
-  e.qkv.q = p.q();
-  e.qkv.kc = reinterpret_cast<typename KP::elem*>(p.kc(l));
-  e.qkv.vc = reinterpret_cast<typename KP::elem*>(p.vc(l));
-  e.qkv.bt = p.bt();
-  e.qkv.rope = p.rope();
-  e.qkv.rows = sp;
-  e.o = {n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(2))};
-  e.gu = {n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(3))};
-  e.down = {n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-
-  const dim3 grid(m->layer_grid);
-  const bool wide = wide_gate_up(d);
-#define SPR_LAYER(HD, JTV, WIDE) k_decode_layer<P, KP, HD, JTV, WIDE><<<grid, 256, 0, m->st>>>(a, e)
-  if (d.hd == 128) {
-    if (JT == 1) wide ? SPR_LAYER(128, 1, true) : SPR_LAYER(128, 1, false);
-    else wide ? SPR_LAYER(128, 2, true) : SPR_LAYER(128, 2, false);
-  } else {
-    if (JT == 1) wide ? SPR_LAYER(64, 1, true) : SPR_LAYER(64, 1, false);
-    else wide ? SPR_LAYER(64, 2, true) : SPR_LAYER(64, 2, false);
-  }
-#undef SPR_LAYER
-  SPR_LAUNCHED(m, "k_decode_layer");
-  return SPR_OK;
-}
-
-// Work-groups per CU of the persistent layer launch: three where every
-// instantiation this model can use fits three (they then run the phases with
-// the per-kernel launch shapes), fewer if not; 0 = unavailable.
-template <class P, class KP, int HD, bool WIDE>
-int layer_grid_per_cu() {
-  int occ = 1 << 30;
-  auto take = [&](const void* k) {
-    int o = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k, 256, 0) != hipSuccess) o = 0;
-    occ = std::min(occ, o);
-  };
-  take(reinterpret_cast<const void*>(&k_decode_layer<P, KP, HD, 1, WIDE>));
-  take(reinterpret_cast<const void*>(&k_decode_layer<P, KP, HD, 2, WIDE>));
-  return std::min(occ, 3);
-}
-template <class P, class KP>
-int layer_grid_per_cu(const spr::Dims& d) {
-  const bool w = wide_gate_up(d);
-  if (d.hd == 128) return w ? layer_grid_per_cu<P, KP, 128, true>() : layer_grid_per_cu<P, KP, 128, false>();
-  return w ? layer_grid_per_cu<P, KP, 64, true>() : layer_grid_per_cu<P, KP, 64, false>();
 }
 
 // Decode attention work-groups resident per CU (0 = unavailable).
@@ -409,6 +306,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     ea.tok_dev = tok_in;
     ea.x = p.x();
     ea.act = p.act(0);
+    ea.err = m->err_dev;
     ea.n_rows = n;
     ea.d = d.d;
     ea.V = d.V;
@@ -449,26 +347,8 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
   for (int r = 0; r < n; ++r)
     while (ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw) > kMergeChunk) ++bpw;
 
-  // A pass of at most 32 rows runs each layer as one persistent launch
-  // (decode mode 1); a timed-out grid barrier of an earlier launch fails the
-  // model here.
-  if (m->err_host != nullptr && *reinterpret_cast<volatile int*>(m->err_host) != 0) {
-    m->sticky = true;
-    return fail(SPR_ERR_HIP, "decode: a persistent layer launch timed out at a grid barrier");
-  }
-  const bool persistent = m->decode_mode == 1 && m->layer_grid > 0 && JT <= 2;
-  // The persistent grid runs the attention work items (flat splits x KV
-  // heads) in one round only if there are at most as many as work-groups:
-  // longer runs per wave instead of a second round.
-  if (persistent)
-    while (count_splits(bpw) * d.Hkv > m->layer_grid && count_splits(bpw) > n) ++bpw;
-
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
-    if (persistent) {
-      if ((st = launch_layer<P, KP>(m, l, rs, sp, JT, bpw)) != SPR_OK) return st;
-      continue;
-    }
     {
       EpiQKV<P, KP> e{};
       e.n_rows = n;
@@ -520,6 +400,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     a.part = p.amax();
     a.tok_dev = tok_out;
     a.n_tiles = d.nt_lm;
+    a.err = m->err_dev;
     std::memcpy(a.slot, rs.slot, sizeof(a.slot));
     std::memcpy(a.out_row, rs.out_row, sizeof(a.out_row));
     std::memcpy(a.hist_idx, rs.hist_idx, sizeof(a.hist_idx));
@@ -684,6 +565,7 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
     a.part = p.amax();
     a.tok_dev = tok;
     a.n_tiles = d.nt_lm;
+    a.err = m->err_dev;
     for (int k = 0; k < kRows; ++k) {
       a.slot[k] = k < n ? ch.emit_slot[k] : 0;
       a.out_row[k] = k < n ? ch.emit_out[k] : -1;
@@ -709,9 +591,24 @@ spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, in
                                    : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, hist);
 }
 
-spr_status check_model(const spr_model* m) {
+// Device check bits (EmbedArgs / ArgmaxArgs `err`), reported by the next call.
+std::string device_check_message(int bits) {
+  std::string s = "a device check failed on an earlier call:";
+  if (bits & kErrTokenRange) s += " a token id outside [0, vocab) was fed (it was read as a clamped id);";
+  if (bits & kErrLogits) s += " a logits row had no finite maximum (its token was set to 0);";
+  return s + " the model's state is unreliable; release it";
+}
+
+spr_status check_model(spr_model* m) {
   if (m == nullptr) return fail(SPR_ERR_INVALID_ARG, "model is null");
-  if (m->sticky) return fail(SPR_ERR_HIP, "an earlier HIP error left the model unusable; release it");
+  if (m->sticky == SPR_OK && m->err_host != nullptr) {
+    const int bits = *reinterpret_cast<volatile int*>(m->err_host);
+    if (bits != 0) {
+      m->sticky = SPR_ERR_DEVICE_CHECK;
+      m->sticky_msg = device_check_message(bits);
+    }
+  }
+  if (m->sticky != SPR_OK) return fail(m->sticky, m->sticky_msg);
   return SPR_OK;
 }
 
@@ -938,25 +835,18 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
   if (e == hipSuccess) e = hipMemsetAsync(p.cnt(), 0, static_cast<size_t>(spr::kMaxRows) * d.Hkv * sizeof(int32_t), m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.act(1), 0, lay.act_bytes, m->st);
   if (e == hipSuccess) e = hipMemsetAsync(p.x(), 0, static_cast<size_t>(spr::kPrefillRows) * d.d * sizeof(float), m->st);
-  if (e == hipSuccess) e = hipMemsetAsync(p.act(2), 0, lay.dec_act_bytes, m->st);
-  if (e == hipSuccess) e = hipMemsetAsync(p.act(3), 0, lay.dec_act_bytes, m->st);
-  if (e == hipSuccess) e = hipMemsetAsync(p.bar(), 0, spr::kBarBytes, m->st);
-  // Persistent layer launch: grid = CUs x work-groups per CU, and the
-  // barrier-timeout flag in mapped pinned host memory (zero-copy: the device
-  // writes it only on a timeout, the host reads it before every pass).
-  if (e == hipSuccess && (d.hd == 64 || d.hd == 128)) {
-    const int per_cu = d.dtype == SPR_F32 ? layer_grid_per_cu<F32, F32>(d)
-                       : d.kv_dtype == SPR_BF16 ? layer_grid_per_cu<BF16, BF16>(d)
-                                                : layer_grid_per_cu<BF16, F32>(d);
+  // The device error flag: mapped pinned host memory, written by kernels only
+  // when a check fails and read by the host at the start of every call.
+  if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->err_host), sizeof(int), hipHostMallocMapped);
+  if (e == hipSuccess) {
+    *m->err_host = 0;
+    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&m->err_dev), m->err_host, 0);
+  }
+  // Decode attention sizes its KV splits by the work-groups resident at once.
+  if (e == hipSuccess) {
     int dev = 0, ncu = 0;
     e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->err_host), sizeof(int), hipHostMallocMapped);
-    if (e == hipSuccess) {
-      *m->err_host = 0;
-      e = hipHostGetDevicePointer(reinterpret_cast<void**>(&m->err_dev), m->err_host, 0);
-    }
-    if (e == hipSuccess && per_cu >= 1) m->layer_grid = per_cu * ncu;
     const int attn_per_cu = d.dtype == SPR_F32 ? attn_blocks_per_cu<F32, F32>(d)
                             : d.kv_dtype == SPR_BF16 ? attn_blocks_per_cu<BF16, BF16>(d)
                                                      : attn_blocks_per_cu<BF16, F32>(d);
@@ -1101,25 +991,22 @@ spr_status spr_export_weight_rows(spr_model* m, int32_t tensor, int32_t layer, i
   return SPR_OK;
 }
 
-spr_status spr_set_decode_mode(spr_model* m, int32_t mode) {
+spr_status spr_test_write_lm_head_row(spr_model* m, int32_t dst, int32_t src, float fill) {
   g_err.clear();
   spr_status st = check_model(m);
   if (st != SPR_OK) return st;
-  if (mode != 0 && mode != 1) return fail(SPR_ERR_INVALID_ARG, "set_decode_mode: mode must be 0 or 1");
-  if (mode == 1 && m->layer_grid <= 0)
-    return fail(SPR_ERR_INVALID_ARG, "set_decode_mode: the persistent layer launch is unavailable for this model here");
-  m->decode_mode = mode;
-  return SPR_OK;
-}
-
-spr_status spr_test_barrier_timeout(spr_model* m, int32_t spin_limit, int32_t skew) {
-  g_err.clear();
-  spr_status st = check_model(m);
-  if (st != SPR_OK) return st;
-  if (spin_limit < 64 || spin_limit > sprk::kBarSpinLimit || skew < 0)
-    return fail(SPR_ERR_INVALID_ARG, "test_barrier_timeout: spin_limit in [64, 2^20] and skew >= 0");
-  m->bar_spin_limit = spin_limit;
-  m->bar_skew = static_cast<unsigned>(skew);
+  const spr::Dims& d = m->d;
+  if (dst < 0 || dst >= d.V || src >= d.V)
+    return fail(SPR_ERR_INVALID_ARG, "test_write_lm_head_row: dst in [0, vocab), src < vocab");
+  Ptrs p{m->ws, &m->lay};
+  if (d.dtype == SPR_BF16)
+    k_write_tiled_row<BF16><<<ceil_div(d.d, 256), 256, 0, m->st>>>(reinterpret_cast<uint16_t*>(p.wlm()), d.kb_d, d.d,
+                                                                    dst, src, fill);
+  else
+    k_write_tiled_row<F32><<<ceil_div(d.d, 256), 256, 0, m->st>>>(reinterpret_cast<float*>(p.wlm()), d.kb_d, d.d, dst,
+                                                                   src, fill);
+  SPR_LAUNCHED(m, "k_write_tiled_row");
+  SPR_HIP(m, hipStreamSynchronize(m->st));
   return SPR_OK;
 }
 

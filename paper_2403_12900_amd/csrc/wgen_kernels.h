@@ -120,4 +120,20 @@ __global__ __launch_bounds__(256) void k_export_rowmajor(const typename P::elem*
   out[i] = P::to_f32(w[static_cast<int64_t>(row0) * cols + i]);
 }
 
+// Overwrites LM-head row dst of the tiled matrix (one thread per element of
+// the row): with row src when src >= 0, else with `fill` rounded to the
+// storage format.  A test aid (planted ties, poisoned rows).
+template <class P>
+__global__ __launch_bounds__(256) void k_write_tiled_row(typename P::elem* __restrict__ w, int KB, int K, int dst,
+                                                         int src, float fill) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= K) return;
+  const int kb = c / P::kblk, kk = c % P::kblk;
+  auto at = [&](int n) {
+    const int lane = (n & 15) + 16 * (kk / P::per16);
+    return ((static_cast<int64_t>(n >> 4) * KB + kb) * 64 + lane) * P::per16 + kk % P::per16;
+  };
+  w[at(dst)] = src >= 0 ? w[at(src)] : P::from_f32(fill);
+}
+
 }  // namespace sprk

@@ -29,8 +29,7 @@ class DeviceRun:
     """
 
     def __init__(self, model: ModelConfig, seed: int, prompts: Sequence[Sequence[int]], stops: Sequence[int],
-                 record: str | set = "all", max_ctx: Optional[int] = None, kv_blocks: Optional[int] = None,
-                 decode_mode: int = 0):
+                 record: str | set = "all", max_ctx: Optional[int] = None, kv_blocks: Optional[int] = None):
         import torch
         from paper_2403_12900_amd.binding import DecodeModel
         B = len(prompts)
@@ -39,8 +38,6 @@ class DeviceRun:
         max_ctx = max_ctx or need
         blocks = sum((s + L - 1 + 15) // 16 for s, L in zip(seq, stops))
         self.m = DecodeModel(model, seed, max_slots=B, max_ctx=max_ctx, kv_blocks=kv_blocks or blocks)
-        if decode_mode:
-            self.m.set_decode_mode(decode_mode)
         tok = self.m.new_token_buffer()
         want0 = record == "all" or 0 in record
         l0, retired = self.m.prefill(list(range(B)), prompts, stops, tok, want_logits=want0)

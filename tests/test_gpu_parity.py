@@ -155,75 +155,6 @@ def test_toy_shapes(case):
     run.close()
 
 
-@pytest.mark.parametrize("case", sorted(TOY_CASES))
-def test_toy_shapes_persistent_layer(case):
-    """The same cases with each layer as one persistent launch (decode mode 1; passes of more than 32
-    rows fall back to one launch per kernel)."""
-    m, plens, stops = TOY_CASES[case]
-    say(f"toy {case}, persistent layer")
-    rng = np.random.default_rng(zlib.crc32(case.encode()))
-    prompts = _prompts(rng, m.vocab, plens)
-    run = DeviceRun(m, 77, prompts, stops, decode_mode=1)
-    assert run.active == R.active_schedule(stops)
-    w = R.Weights(oracle_shape(m), 77)
-    st = check_against_oracle(run, w, prompts, stops, range(len(prompts)), *_tol(m))
-    say(case, st)
-    run.close()
-
-
-def test_persistent_layer_equals_per_kernel_7b():
-    """Llama-2-7B shape, 32 ragged requests (passes of 1..32 rows): one persistent launch per layer computes
-    every projection tile with the same per-wave K split and reduction order as one launch per kernel; only
-    the attention's KV splits differ (the persistent grid runs all of a pass's splits in one round), which
-    changes the order of the softmax merge.  Logits agree to 1e-2 (a fifth of the oracle tolerance), and
-    tokens agree except where the top two logits are that close."""
-    cfg = CONFIGS["c3"]
-    wl = make_workload(cfg)
-    stops = [int(min(s, 12)) for s in wl.stop_lens]
-    record = {0, 1, 5, 11}
-    say("7B persistent vs per-kernel: 32 requests, stops <= 12")
-    a = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops, record="all", decode_mode=0)
-    b = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops, record=record, decode_mode=1)
-    worst, diverged = 0.0, 0
-    for i in range(len(stops)):
-        d = next((s for s in range(stops[i]) if a.tokens[i][s] != b.tokens[i][s]), None)
-        if d is not None:
-            z = a.logits[i][d]
-            assert z.max() - z[b.tokens[i][d]] <= 2e-2, (i, d)      # a near-tie only
-            diverged += 1
-            continue
-        for s, z in b.logits[i].items():
-            worst = max(worst, float(np.abs(z - a.logits[i][s]).max()))
-    say("7B persistent vs per-kernel: max |dz|", worst, "diverged at near-ties:", diverged)
-    assert worst <= 1e-2 and diverged <= 2
-    a.close()
-    b.close()
-
-
-def test_persistent_layer_barrier_timeout_fails_the_next_call():
-    """A persistent launch whose grid barriers cannot complete (forced from the host: its barrier generation is
-    shifted and the poll limit cut to 64) still ends, and the next call on the model reports the timeout."""
-    import torch
-    from paper_2403_12900_amd.binding import DecodeModel, SproutError, SPR_ERR_HIP, SPR_ERR_INVALID_ARG
-    m, _, _ = TOY_CASES["bf16_mha_hd64_ragged"]
-    dm = DecodeModel(m, 78, max_slots=2, max_ctx=64)
-    dm.set_decode_mode(1)
-    tok = dm.new_token_buffer()
-    rng = np.random.default_rng(3)
-    dm.prefill([0, 1], _prompts(rng, m.vocab, [9, 20]), [6, 6], tok)
-    with pytest.raises(SproutError) as bad:
-        dm.test_barrier_timeout(8, 1)
-    assert bad.value.status == SPR_ERR_INVALID_ARG
-    dm.decode_step([0, 1], [9, 20], tok)                  # healthy
-    dm.test_barrier_timeout(64, 1000)
-    dm.decode_step([0, 1], [10, 21], tok)                 # enqueued; its barriers give up after 64 polls
-    torch.cuda.synchronize()
-    with pytest.raises(SproutError) as failed:
-        dm.decode_step([0, 1], [11, 22], tok)
-    assert failed.value.status == SPR_ERR_HIP and "grid barrier" in str(failed.value)
-    dm.close()
-
-
 def test_fragmented_kv_reservation():
     """Paged KV with a fragmented reservation: slots 0-2 reserve blocks [0,1], [2,3], [4,5]; slot 1 is
     freed and refilled with a longer prompt, which reserves [2,3,6,7].  Teacher-forced logits of all three
