@@ -263,33 +263,51 @@ def forward_causal(w: Weights, tokens: Sequence[int], want_positions: Optional[S
     ``n_layers`` truncates the model (used only by pins on toy shapes);
     ``progress(layer)`` is called after each layer if given.
     """
+    return forward_causal_requests(w, [tokens], [want_positions], n_layers=n_layers, progress=progress)[0]
+
+
+def forward_causal_requests(w: Weights, seqs: Sequence[Sequence[int]],
+                            want_positions: Optional[Sequence[Optional[Sequence[int]]]] = None,
+                            n_layers: Optional[int] = None, progress=None) -> List[np.ndarray]:
+    """forward_causal for several independent requests: request i's tokens sit at positions
+    0..len(seqs[i])-1 and it attends only to its own positions.  The row-wise steps (norms,
+    projections, MLP) take all requests' rows in one product per matrix, so each layer's weights
+    are drawn once for all of them; the result for a request is the same as forward_causal's.
+    Returns one [len(want_positions[i]), V] array per request (all positions when None)."""
     sh = w.shape
-    tokens = np.asarray(tokens, dtype=np.int64)
-    T = len(tokens)
-    pos = np.arange(T)
+    seqs = [np.asarray(t, dtype=np.int64) for t in seqs]
+    if want_positions is None:
+        want_positions = [None] * len(seqs)
+    lens = [len(t) for t in seqs]
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
     g = w.gain()
-    x = embed_rows(w, tokens)
+    x = embed_rows(w, np.concatenate(seqs)) if seqs else np.zeros((0, sh.d_model))
     L = sh.n_layers if n_layers is None else n_layers
     for layer in range(L):
         W = w.layer(layer)
         a = rmsnorm(x, g, sh.rms_eps)
-        q = (a @ W["wq"].T).reshape(T, sh.n_heads, sh.head_dim)
-        k = (a @ W["wk"].T).reshape(T, sh.n_kv_heads, sh.head_dim)
-        v = (a @ W["wv"].T).reshape(T, sh.n_kv_heads, sh.head_dim)
-        q = apply_rope(q, pos, sh.rope_base)
-        k = apply_rope(k, pos, sh.rope_base)
-        k, v = cache_kv(sh, k, v)
-        o = causal_attention(q, k, v).reshape(T, sh.n_heads * sh.head_dim)
+        q_all, k_all, v_all = a @ W["wq"].T, a @ W["wk"].T, a @ W["wv"].T
+        o = np.empty((x.shape[0], sh.n_heads * sh.head_dim))
+        for i, T in enumerate(lens):
+            r = slice(off[i], off[i + 1])
+            pos = np.arange(T)
+            q = apply_rope(q_all[r].reshape(T, sh.n_heads, sh.head_dim), pos, sh.rope_base)
+            k = apply_rope(k_all[r].reshape(T, sh.n_kv_heads, sh.head_dim), pos, sh.rope_base)
+            k, v = cache_kv(sh, k, v_all[r].reshape(T, sh.n_kv_heads, sh.head_dim))
+            o[r] = causal_attention(q, k, v).reshape(T, sh.n_heads * sh.head_dim)
         x = x + o @ W["wo"].T
         m = rmsnorm(x, g, sh.rms_eps)
         x = x + swiglu(m, W["w1"], W["w3"], W["w2"])
         del W
         if progress is not None:
             progress(layer)
-    if want_positions is None:
-        want_positions = range(T)
-    xs = rmsnorm(x[np.asarray(want_positions, dtype=np.int64)], g, sh.rms_eps)
-    return xs @ w.matrix("lm_head").T
+    lm = w.matrix("lm_head")
+    out = []
+    for i, T in enumerate(lens):
+        want = range(T) if want_positions[i] is None else want_positions[i]
+        xs = rmsnorm(x[off[i] + np.asarray(want, dtype=np.int64)], g, sh.rms_eps)
+        out.append(xs @ lm.T)
+    return out
 
 
 def teacher_forced_logits(w: Weights, prompt: Sequence[int], generated: Sequence[int],
@@ -300,14 +318,23 @@ def teacher_forced_logits(w: Weights, prompt: Sequence[int], generated: Sequence
     at position n + s - 1.  The sequence run is prompt ++ generated[:-1], so
     the oracle sees exactly the tokens the device saw.
     """
-    n = len(prompt)
-    Lg = len(generated)
+    return teacher_forced_logits_requests(w, [prompt], [generated], [steps], progress=progress)[0]
+
+
+def teacher_forced_logits_requests(w: Weights, prompts: Sequence[Sequence[int]],
+                                   generated: Sequence[Sequence[int]],
+                                   steps: Optional[Sequence[Optional[Sequence[int]]]] = None,
+                                   progress=None) -> List[np.ndarray]:
+    """teacher_forced_logits for several requests in one pass over the layers."""
     if steps is None:
-        steps = range(Lg)
-    steps = list(steps)
-    last = max(steps)
-    seq = list(prompt) + list(generated[:last])
-    return forward_causal(w, seq, [n - 1 + s for s in steps], progress=progress)
+        steps = [None] * len(prompts)
+    seqs, want = [], []
+    for p, gen, st in zip(prompts, generated, steps):
+        st = list(range(len(gen))) if st is None else list(st)
+        n = len(p)
+        seqs.append(list(p) + list(gen[:max(st)]))
+        want.append([n - 1 + s for s in st])
+    return forward_causal_requests(w, seqs, want, progress=progress)
 
 
 # --------------------------------------------------------------------------

@@ -68,8 +68,7 @@ def _cached(run: str, kv64: np.ndarray, kv32: np.ndarray) -> np.ndarray:
 
 def lockstep_logits(shape: R.Shape, seed: int, tokens: Sequence[int], runs: Sequence[str] = RUNS,
                     progress=None) -> Dict[str, np.ndarray]:
-    """Logits [T, V] at every position of `tokens` for each run, plus per-run counts of cached
-    elements whose stored value differs from the bf16_f64 (or f32_f64) run's."""
+    """Logits [T, V] at every position of `tokens` for each run."""
     sh = shape
     w = R.Weights(sh, seed, resident=False)
     tokens = np.asarray(tokens, dtype=np.int64)
@@ -86,8 +85,8 @@ def lockstep_logits(shape: R.Shape, seed: int, tokens: Sequence[int], runs: Sequ
         k64 = (A @ W["wk"].T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         v64 = (A @ W["wv"].T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         A32 = A.astype(np.float32)
-        k32 = (A32 @ W["wk"].T.astype(np.float32)).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
-        v32 = (A32 @ W["wv"].T.astype(np.float32)).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
+        k32 = (A32 @ W["wk"].astype(np.float32).T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
+        v32 = (A32 @ W["wv"].astype(np.float32).T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         O = np.empty((nr, T, sh.n_heads * sh.head_dim))
         for i, r in enumerate(runs):
             qi = R.apply_rope(q[i], pos, sh.rope_base)

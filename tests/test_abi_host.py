@@ -17,7 +17,8 @@ from paper_2403_12900_amd.configs import CONFIGS, LLAMA2_7B, TINY
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "sprout.h")
-HOST_LIB = os.path.join(ROOT, "paper_2403_12900_amd", "libsprout_host.so")
+# SPROUT_HOST_LIB selects another build of the same sources (the sanitizer build).
+HOST_LIB = os.environ.get("SPROUT_HOST_LIB", os.path.join(ROOT, "paper_2403_12900_amd", "libsprout_host.so"))
 
 
 def declared_functions():

@@ -109,6 +109,11 @@ TOY_CASES = {
         ModelConfig(n_layers=2, d_model=256, n_heads=8, n_kv_heads=1, head_dim=128, d_ff=344, vocab=500,
                     kv_bf16=False),
         [40, 3, 17, 90, 1], [5, 9, 2, 4, 6]),
+    # One row of ~1700 positions at hd128 with 4 query heads per KV head: 107 blocks would be 27
+    # one-block-per-wave splits, past the 16 one merge round takes, so the run per wave grows.
+    "bf16_gqa4_hd128_long_context": (
+        ModelConfig(n_layers=2, d_model=256, n_heads=8, n_kv_heads=2, head_dim=128, d_ff=344, vocab=500),
+        [1690, 30, 5], [12, 4, 2]),
     "bf16_long_context_splits": (
         ModelConfig(n_layers=2, d_model=128, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=128, vocab=500),
         [700, 300], [20, 3]),
@@ -281,69 +286,61 @@ def test_batch_invariance():
     full.close()
 
 
-# ------------------------------------------------------------------ Llama-2-7B shape, ragged batch 32
+# ------------------------------------------------------------------ full-size configurations
 
-def test_llama2_7b_ragged_batch32_sampled():
-    """The benchmarked workload at full size: all 32 requests decode to their
-    stop lengths; the oracle checks the two shortest requests at every step it
-    can afford (prefill, early, middle and final steps)."""
-    cfg = CONFIGS["c3"]
-    wl = make_workload(cfg)
-    seq, stops = wl.seq_lens, wl.stop_lens
-    order = np.argsort(seq + stops)
-    sampled = [int(order[0]), int(order[1])]
-    steps = {}
-    for i in sampled:
-        L = int(stops[i])
-        steps[i] = sorted({0, 1, 2, L // 2, L - 2, L - 1} & set(range(L)))
-    record = set().union(*steps.values())
-    say(f"7B ragged batch 32: sampled requests {sampled}, steps {steps}")
-    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops.tolist(), record=record)
-    assert run.active == R.active_schedule(stops.tolist())
-    assert [len(t) for t in run.tokens] == stops.tolist()
-    w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed, resident=False)
-    st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL, steps_of=lambda i: steps[i])
-    say("c3 sampled", st)
-    assert st["rows"] == sum(len(v) for v in steps.values())
-    run.close()
-
-
-# ------------------------------------------------------------------ the other full-size configurations
-
-def _sampled_full_size(key, n_requests, extra_steps=()):
+def _full_size(key, pick):
+    """The configuration's whole closed batch decodes on the device, free-running, to every request's
+    stop length; the requests `pick(context lengths)` names are compared with the oracle at every step
+    (prefill included), all of them in one oracle pass over the layers."""
     cfg = CONFIGS[key]
     wl = make_workload(cfg)
     seq, stops = wl.seq_lens, wl.stop_lens
-    order = np.argsort(seq + stops)
-    sampled = [int(i) for i in order[:n_requests]]
-    steps = {}
-    for i in sampled:
-        L = int(stops[i])
-        steps[i] = sorted(({0, 1, 2, L // 2, L - 2, L - 1} | set(extra_steps)) & set(range(L)))
-    record = set().union(*steps.values())
-    say(f"{cfg.name}: sampled requests {sampled}, steps {steps}")
-    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops.tolist(), record=record)
+    ctx = seq + stops - 1
+    sampled = sorted(set(int(i) for i in pick(ctx)))
+    record = set(range(int(max(stops[i] for i in sampled))))
+    say(f"{cfg.name}: checking requests {sampled} (contexts {[int(ctx[i]) for i in sampled]}) at every step")
+    run = DeviceRun(cfg.model, cfg.weight_seed, wl.tokens, stops.tolist(), record=record, keep=set(sampled))
     assert run.active == R.active_schedule(stops.tolist())
     assert [len(t) for t in run.tokens] == stops.tolist()
     say(f"{cfg.name}: device decode done; oracle")
     w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed, resident=False)
-    st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL, steps_of=lambda i: steps[i])
+    st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL)
     say(cfg.name, st)
-    assert st["rows"] == sum(len(v) for v in steps.values())
+    assert st["rows"] == int(sum(stops[i] for i in sampled))
+    assert st["max_context"] == int(max(ctx[i] for i in sampled)) + 1
     run.close()
+    return st
+
+
+def _shortest(ctx, n):
+    return [int(i) for i in np.argsort(ctx, kind="stable")[:n]]
+
+
+def _nearest(ctx, target):
+    return int(np.argmin(np.abs(ctx - target)))
+
+
+def test_llama2_7b_ragged_batch32():
+    """The benchmarked workload at full size: all 32 requests decode to their stop lengths.  Checked at
+    every step: the request with the longest context (616-token prompt, 1020 generated, 1635 positions
+    at its last step -- it decodes alone for half of the batch's steps), the one nearest the median
+    context, and the two shortest."""
+    _full_size("c3", lambda ctx: _shortest(ctx, 2) + [int(np.argmax(ctx)), _nearest(ctx, np.median(ctx))])
 
 
 def test_llama2_7b_batch1_256_tokens():
-    """The latency case: one request, prompt 128, 256 generated tokens, checked at spread-out steps."""
-    _sampled_full_size("c2", 1, extra_steps=(64, 127, 200))
+    """The latency case: one request, prompt 128, 256 generated tokens, every step checked."""
+    _full_size("c2", lambda ctx: [0])
 
 
-def test_llama2_13b_ragged_batch64_sampled():
-    """13B shape, 64 ragged requests in 16-position KV pages; the two shortest requests are checked."""
-    _sampled_full_size("c4", 2)
+def test_llama2_13b_ragged_batch64():
+    """13B shape, 64 ragged requests in 16-position KV pages: the longest context (1353 positions) and
+    the two shortest are checked at every step."""
+    _full_size("c4", lambda ctx: _shortest(ctx, 2) + [int(np.argmax(ctx))])
 
 
-def test_llama2_70b_gqa_ragged_batch16_sampled():
-    """70B shape with grouped-query attention (8 query heads per KV head), ~138 GB of weights on one GPU;
-    the shortest request is checked against the oracle (which streams the weights layer by layer)."""
-    _sampled_full_size("c5", 1)
+def test_llama2_70b_gqa_ragged_batch16():
+    """70B shape with grouped-query attention (8 query heads per KV head), ~138 GB of weights on one
+    GPU: the request nearest the median context (884 positions) and the shortest are checked at every
+    step against the oracle, which streams the weights layer by layer."""
+    _full_size("c5", lambda ctx: _shortest(ctx, 1) + [_nearest(ctx, np.median(ctx))])

@@ -396,3 +396,15 @@ def test_retirement_closed_form():
         assert act == sorted(i for i in range(len(stops)) if stops[i] > s)
     assert sum(len(a) for a in sched) == sum(L - 1 for L in stops)
     assert R.active_schedule([1, 1]) == []
+
+
+def test_requests_share_layers_without_mixing():
+    """forward_causal_requests gives each request what forward_causal gives it alone (requests stacked
+    into one product per matrix must not see each other's positions)."""
+    w = R.Weights(TOY, 21)
+    rng = np.random.default_rng(31)
+    seqs = [rng.integers(0, TOY.vocab, size=n).tolist() for n in (7, 1, 12)]
+    want = [[0, 6], None, [3, 11]]
+    got = R.forward_causal_requests(w, seqs, want)
+    for s, wp, g in zip(seqs, want, got):
+        assert np.allclose(g, R.forward_causal(w, s, wp), rtol=1e-12, atol=1e-12)

@@ -18,7 +18,8 @@ from paper_2403_12900_amd import binding
 from paper_2403_12900_amd.configs import TINY
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HOST_LIB = os.path.join(ROOT, "paper_2403_12900_amd", "libsprout_host.so")
+# SPROUT_HOST_LIB selects another build of the same sources (the sanitizer build).
+HOST_LIB = os.environ.get("SPROUT_HOST_LIB", os.path.join(ROOT, "paper_2403_12900_amd", "libsprout_host.so"))
 I32 = ctypes.POINTER(ctypes.c_int32)
 
 
