@@ -161,6 +161,21 @@ struct Ptrs {
   float* rs() const { return reinterpret_cast<float*>(ws + l->off_rs); }
 };
 
+// Per-pass scratch of a decode forward: attention split partials (at most
+// max_splits splits), split arrival counters (zero between launches) and the
+// LM head's per-tile greedy candidates (regions of the model's workspace).
+struct DecodeScratch {
+  float* part;
+  int32_t* cnt;
+  float2* amax;
+  int max_splits;
+};
+
+DecodeScratch workspace_scratch(const spr_model* m) {
+  Ptrs p{m->ws, &m->lay};
+  return DecodeScratch{p.part(), p.cnt(), p.amax(), spr::kMaxSplits};
+}
+
 template <class P>
 spr_status init_weights(spr_model* m) {
   const spr::Dims& d = m->d;
@@ -249,7 +264,8 @@ spr_status launch_attention(spr_model* m, const AttnArgs& a) {
 
 // Attention arguments of one layer over rs (kv splits of bpw blocks per wave).
 template <class P, class KP>
-AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int Rp, int bpw, void* act) {
+AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos& sp, int Rp, int bpw, void* act,
+                        const DecodeScratch& sc) {
   const spr::Dims& d = m->d;
   Ptrs p{m->ws, &m->lay};
   AttnArgs a{};
@@ -258,8 +274,8 @@ AttnArgs attention_args(spr_model* m, int l, const RowSet& rs, const RowSlotPos&
   a.vc = p.vc(l);
   a.bt = p.bt();
   a.act = act;
-  a.part = p.part();
-  a.cnt = p.cnt();
+  a.part = sc.part;
+  a.cnt = sc.cnt;
   a.n_rows = rs.n;
   a.H = d.H;
   a.Hkv = d.Hkv;
@@ -289,7 +305,7 @@ int attn_blocks_per_cu(const spr::Dims& d) {
 // rows write their greedy token to tok_out[slot].
 template <class P, class KP>
 spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
-                   int32_t* hist) {
+                   int32_t* hist, const DecodeScratch& sc) {
   const spr::Dims& d = m->d;
   Ptrs p{m->ws, &m->lay};
   const int n = rs.n;
@@ -340,7 +356,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     while (count_splits(fit) * d.Hkv > m->attn_slots && count_splits(fit) > n && fit < 2 * bpw) ++fit;
     if (count_splits(fit) * d.Hkv <= m->attn_slots) bpw = fit;
   }
-  while (count_splits(bpw) > spr::kMaxSplits) ++bpw;
+  while (count_splits(bpw) > sc.max_splits) ++bpw;
   // A row's splits are merged by its last arriving split, kMergeChunk
   // partials per round of loads: keep every row within one round (measured
   // on 7B at one row of 1024 positions: 17 splits 11.5 us, 9 splits 10.1 us).
@@ -367,7 +383,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       if ((st = launch_gemm<P>(m, d.nt_qkv, p.wqkv(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
     }
     {
-      const AttnArgs a = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1));
+      const AttnArgs a = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1), sc);
       st = d.hd == 128 ? launch_attention<P, KP, 128>(m, a) : launch_attention<P, KP, 64>(m, a);
       if (st != SPR_OK) return st;
     }
@@ -391,13 +407,13 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     e.dnorm = d.d;
     e.eps = d.eps;
     e.logits = logits;
-    e.part = p.amax();
+    e.part = sc.amax;
     std::memcpy(e.out_row, rs.out_row, sizeof(e.out_row));
     if ((st = launch_gemm<P>(m, d.nt_lm, p.wlm(), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
   }
   {
     ArgmaxArgs a{};
-    a.part = p.amax();
+    a.part = sc.amax;
     a.tok_dev = tok_out;
     a.n_tiles = d.nt_lm;
     a.err = m->err_dev;
@@ -585,10 +601,10 @@ spr_status prefill_any(spr_model* m, const PrefillChunk& ch, int32_t* tok, float
 }
 
 spr_status forward_any(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_t* tok_out, float* logits,
-                       int32_t* hist) {
-  if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, hist);
-  return m->d.kv_dtype == SPR_BF16 ? forward<BF16, BF16>(m, rs, tok_in, tok_out, logits, hist)
-                                   : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, hist);
+                       int32_t* hist, const DecodeScratch& sc) {
+  if (m->d.dtype == SPR_F32) return forward<F32, F32>(m, rs, tok_in, tok_out, logits, hist, sc);
+  return m->d.kv_dtype == SPR_BF16 ? forward<BF16, BF16>(m, rs, tok_in, tok_out, logits, hist, sc)
+                                   : forward<BF16, F32>(m, rs, tok_in, tok_out, logits, hist, sc);
 }
 
 // Device check bits (EmbedArgs / ArgmaxArgs `err`), reported by the next call.
@@ -739,7 +755,7 @@ struct GpuServe : spr::ServeDevice {
       rs.hist_idx[r] = v ? static_cast<int>(off[req[r]] + produced[r]) : -1;
     }
     for (int i = 0; i < n; ++i) cur.push_back(req[i]);
-    spr_status st = forward_any(m, rs, tok, tok, nullptr, out);
+    spr_status st = forward_any(m, rs, tok, tok, nullptr, out, workspace_scratch(m));
     if (st != SPR_OK || eos_id < 0) return st;
     for (int i = 0; i < n; ++i) rows[par][1].push_back(Row{slots[i], req[i], produced[i]});
     return snapshot(1);
@@ -905,7 +921,7 @@ spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots,
     rs.tok[r] = 0;
     rs.hist_idx[r] = -1;
   }
-  if ((st = forward_any(m, rs, tok, tok, logits, nullptr)) != SPR_OK) return st;
+  if ((st = forward_any(m, rs, tok, tok, logits, nullptr, workspace_scratch(m))) != SPR_OK) return st;
   m->tab.commit_decode(n_active, slots, retired);
   return SPR_OK;
 }

@@ -103,6 +103,12 @@ __global__ __launch_bounds__(256) void k_argmax_final(ArgmaxArgs a) {
   }
 }
 
+// out[0 .. n) = 0.
+__global__ __launch_bounds__(256) void k_zero_i32(int32_t* out, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) out[i] = 0;
+}
+
 // Streaming read of n16 16-byte words with the projections' load form
 // (nontemporal 16-byte loads, kReadUnroll in flight per thread): the read
 // rate this memory path reaches with no arithmetic attached.  Full chunks of

@@ -307,7 +307,7 @@ def _full_size(key, pick):
     st = check_against_oracle(run, w, wl.tokens, stops, sampled, *BF16_TOL)
     say(cfg.name, st)
     assert st["rows"] == int(sum(stops[i] for i in sampled))
-    assert st["max_context"] == int(max(ctx[i] for i in sampled)) + 1
+    assert st["max_context"] == int(max(ctx[i] for i in sampled))   # positions attended at the last step
     run.close()
     return st
 
