@@ -78,6 +78,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.spr_prefill.argtypes = [vp, ctypes.c_int32, _I32P, _I32P, _I32P, _I32P, vp, vp, _I32P]
     L.spr_decode_step.restype = ctypes.c_int
     L.spr_decode_step.argtypes = [vp, ctypes.c_int32, _I32P, _I32P, vp, vp, _I32P]
+    L.spr_decode_step_static_scratch.restype = ctypes.c_int
+    L.spr_decode_step_static_scratch.argtypes = [vp, ctypes.c_int32, _I32P, _I32P, vp, vp, _I32P]
     L.spr_rewind_slot.restype = ctypes.c_int
     L.spr_rewind_slot.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
     L.spr_free_slot.restype = ctypes.c_int
@@ -182,6 +184,18 @@ class DecodeModel:
         _check(self.lib.spr_decode_step(self.h, n, _ptr(sl), _ptr(ln), ctypes.c_void_p(tok.data_ptr()),
                                         ctypes.c_void_p(logits.data_ptr() if want_logits else 0), _ptr(retired)))
         return (logits if want_logits else None), retired
+
+    def decode_step_static_scratch(self, slots: Sequence[int], lens: Sequence[int], tok, want_logits: bool = False):
+        """decode_step whose scratch is the library's static device array (spr_decode_step_static_scratch)."""
+        n = len(slots)
+        sl = _i32(slots)
+        ln = _i32(lens)
+        retired = np.zeros(n, dtype=np.int32)
+        logits = self.torch.empty((n, self.vocab), dtype=self.torch.float32, device=self.device) if want_logits else None
+        _check(self.lib.spr_decode_step_static_scratch(self.h, n, _ptr(sl), _ptr(ln), ctypes.c_void_p(tok.data_ptr()),
+                                                       ctypes.c_void_p(logits.data_ptr() if want_logits else 0),
+                                                       _ptr(retired)))
+        return logits, retired
 
     def rewind(self, slot: int, length: int, produced: int):
         _check(self.lib.spr_rewind_slot(self.h, slot, length, produced))

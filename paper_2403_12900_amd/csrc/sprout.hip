@@ -23,6 +23,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -37,6 +38,18 @@ using namespace sprk;
 
 static_assert(spr::kPrefillRows == sprk::kPrefillRows, "prefill chunk size");
 static_assert(spr::kMaxRows == sprk::kRows, "decode pass size");
+
+// Scratch of spr_decode_step_static_scratch: a fixed array in device memory,
+// one per device that loads the library, held until the process ends.
+// Regions: attention split partials, split arrival counters, LM-head greedy
+// candidates.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in symbol): it resolves the array's device address
+// once per device at init (static_scratch_address) and passes that.
+constexpr size_t kStaticPartBytes = size_t{8} << 20;
+constexpr size_t kStaticCntBytes = size_t{64} << 10;
+constexpr size_t kStaticAmaxBytes = (size_t{8} << 20) - kStaticCntBytes;
+constexpr size_t kStaticScratchBytes = kStaticPartBytes + kStaticCntBytes + kStaticAmaxBytes;  // 16 MiB
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 struct spr_model {
   spr::Dims d{};
@@ -58,6 +71,8 @@ struct spr_model {
   // the next call on the model reports it.
   int* err_host = nullptr;
   int* err_dev = nullptr;
+  // Device address of this device's static scratch array (see `scratch`).
+  char* static_scratch = nullptr;
   ~spr_model() {
     if (err_host != nullptr) (void)hipHostFree(err_host);
   }
@@ -92,6 +107,25 @@ spr_status hip_fail(spr_model* m, const char* what, hipError_t e) {
     hipError_t e_ = hipGetLastError();                 \
     if (e_ != hipSuccess) return hip_fail(m, what, e_); \
   } while (0)
+
+// Device address of `scratch` on each device, resolved once per device with
+// that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_addr[kMaxDevices] = {};
+
+hipError_t static_scratch_address(int dev, char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
 
 uint64_t stream_key(uint64_t seed, int tensor, int layer) {
   return sm_output(seed, 1u + 256u * static_cast<uint64_t>(tensor) + static_cast<uint64_t>(layer));
@@ -163,7 +197,8 @@ struct Ptrs {
 
 // Per-pass scratch of a decode forward: attention split partials (at most
 // max_splits splits), split arrival counters (zero between launches) and the
-// LM head's per-tile greedy candidates (regions of the model's workspace).
+// LM head's per-tile greedy candidates.  Either regions of the model's
+// workspace or of the static scratch array (spr_decode_step_static_scratch).
 struct DecodeScratch {
   float* part;
   int32_t* cnt;
@@ -863,6 +898,7 @@ spr_status spr_init(const spr_config* cfg, uint64_t seed, void* dev_ws, size_t w
     int dev = 0, ncu = 0;
     e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = static_scratch_address(dev, &m->static_scratch);
     const int attn_per_cu = d.dtype == SPR_F32 ? attn_blocks_per_cu<F32, F32>(d)
                             : d.kv_dtype == SPR_BF16 ? attn_blocks_per_cu<BF16, BF16>(d)
                                                      : attn_blocks_per_cu<BF16, F32>(d);
@@ -922,6 +958,46 @@ spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots,
     rs.hist_idx[r] = -1;
   }
   if ((st = forward_any(m, rs, tok, tok, logits, nullptr, workspace_scratch(m))) != SPR_OK) return st;
+  m->tab.commit_decode(n_active, slots, retired);
+  return SPR_OK;
+}
+
+spr_status spr_decode_step_static_scratch(spr_model* m, int32_t n_active, const int32_t* slots, const int32_t* lens,
+                                          int32_t* tok, float* logits, int32_t* retired) {
+  g_err.clear();
+  spr_status st = check_model(m);
+  if (st != SPR_OK) return st;
+  if (slots == nullptr || lens == nullptr || tok == nullptr)
+    return fail(SPR_ERR_INVALID_ARG, "decode_step_static_scratch: slots, lens and tok must not be null");
+  const spr::Dims& d = m->d;
+  const size_t per_split = static_cast<size_t>(d.H) * (d.hd + 4) * sizeof(float);
+  const int max_splits = static_cast<int>(std::min<size_t>(spr::kMaxSplits, kStaticPartBytes / per_split));
+  if (static_cast<size_t>(spr::kMaxRows) * d.Hkv * sizeof(int32_t) > kStaticCntBytes ||
+      static_cast<size_t>(d.nt_lm) * spr::kMaxRows * sizeof(float2) > kStaticAmaxBytes || max_splits < n_active)
+    return fail(SPR_ERR_INVALID_ARG, "decode_step_static_scratch: the model or batch exceeds the 16 MiB static "
+                                     "scratch (at most 128 KV heads, vocab <= 130048, and n_heads * (head_dim + 4) "
+                                     "* 4 * n_active <= 8 MiB)");
+  std::string err;
+  if ((st = m->tab.check_decode(n_active, slots, lens, &err)) != SPR_OK) return fail(st, err);
+  RowSet rs;
+  rs.n = n_active;
+  for (int r = 0; r < kRows; ++r) {
+    const bool v = r < n_active;
+    rs.slot[r] = v ? slots[r] : 0;
+    rs.pos[r] = v ? lens[r] : 0;
+    rs.out_row[r] = v ? r : -1;
+    rs.tok[r] = 0;
+    rs.hist_idx[r] = -1;
+  }
+  DecodeScratch sc{reinterpret_cast<float*>(m->static_scratch),
+                   reinterpret_cast<int32_t*>(m->static_scratch + kStaticPartBytes),
+                   reinterpret_cast<float2*>(m->static_scratch + kStaticPartBytes + kStaticCntBytes), max_splits};
+  // Every call shares the array: the split counters must start at zero (a
+  // fill kernel, which a graph capture may record).
+  const int ncnt = n_active * d.Hkv;
+  k_zero_i32<<<ceil_div(ncnt, 256), 256, 0, m->st>>>(sc.cnt, ncnt);
+  SPR_LAUNCHED(m, "k_zero_i32");
+  if ((st = forward_any(m, rs, tok, tok, logits, nullptr, sc)) != SPR_OK) return st;
   m->tab.commit_decode(n_active, slots, retired);
   return SPR_OK;
 }
