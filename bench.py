@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "decode tokens/s + achieved HBM GB/s, Llama-2-7B-shape bf16, ragged batch 32"
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
-DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16, false>, 2, 8, true>"
+DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16>, 2, 8, true>"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_gemm_pmc_llama2_7b_b8.txt")
 
 
@@ -235,6 +235,26 @@ def trace_summary(trace_dir: str) -> None:
           f"{busy / 1e3:.1f} ms of it in kernels: {(total - busy) / 1e3:.1f} ms between the decode's "
           f"{launches} launches ({(total - busy) / launches:.2f} us each). Per launch in the table: mean "
           f"kernel time and algorithmic GB/s.")
+
+
+def stats_summary(csv_path: str, top: int = 24) -> None:
+    """Prints a rocprofv3 kernel_stats.csv (--kernel-trace --stats) as a markdown table: total and
+    average kernel time per kernel, the `top` kernels by total time."""
+    import csv
+    import re
+    rows = []
+    with open(csv_path) as fh:
+        for r in csv.DictReader(fh):
+            name = re.sub(r"\(.*", "", r["Name"]).replace("sprk::", "").strip()
+            rows.append((float(r["TotalDurationNs"]), int(r["Calls"]), float(r["AverageNs"]), float(r["MinNs"]),
+                         float(r["MaxNs"]), float(r["Percentage"]), name))
+    rows.sort(reverse=True)
+    total = sum(r[0] for r in rows)
+    print(f"Total kernel time {total / 1e6:.1f} ms over {sum(r[1] for r in rows)} launches.\n")
+    print("| total ms | % | calls | avg us | min us | max us | kernel |")
+    print("|---:|---:|---:|---:|---:|---:|---|")
+    for tot, calls, avg, mn, mx, pct, name in rows[:top]:
+        print(f"| {tot / 1e6:.1f} | {pct:.2f} | {calls} | {avg / 1e3:.2f} | {mn / 1e3:.2f} | {mx / 1e3:.2f} | `{name}` |")
 
 
 def step_sweep(key: str, steps: int = 12):
@@ -528,6 +548,8 @@ def main():
                     help="only run the c3 prefill twice (for rocprofv3 --pmc of the prefill GEMMs)")
     ap.add_argument("--decode-probe", action="store_true",
                     help="only run the c3 prefill and one ragged decode (for rocprofv3 --kernel-trace)")
+    ap.add_argument("--stats-summary", metavar="STATS_CSV", default=None,
+                    help="print a rocprofv3 kernel_stats.csv as the markdown table kept under profiles/")
     ap.add_argument("--trace-summary", metavar="TRACE_DIR", default=None,
                     help="print the decode's kernel time by active rows from a --decode-probe kernel trace")
     ap.add_argument("--traffic-probe", action="store_true",
@@ -552,6 +574,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args.trace_summary)
+        return
+    if args.stats_summary:
+        stats_summary(args.stats_summary)
         return
     if args.step_sweep:
         step_sweep(args.step_sweep)
