@@ -292,7 +292,7 @@ spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int K
 
 template <class P, class KP, int HD>
 spr_status launch_attention(spr_model* m, const AttnArgs& a) {
-  k_attn_decode<KP, P, HD><<<dim3(a.split_start[a.n_rows], a.Hkv), 256, 0, m->st>>>(a);
+  k_attn_decode<KP, P, HD><<<dim3(a.Hkv, a.split_start[a.n_rows]), 256, 0, m->st>>>(a);
   SPR_LAUNCHED(m, "k_attn_decode");
   return SPR_OK;
 }
