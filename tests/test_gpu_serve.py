@@ -39,8 +39,8 @@ def _requests(rng, vocab, n):
 def check_tokens_against_oracle(w, prompts, toks, tol):
     ties = 0
     steps = 0
-    for i, (p, g) in enumerate(zip(prompts, toks)):
-        z = R.teacher_forced_logits(w, p, g)
+    zs = R.teacher_forced_logits_requests(w, prompts, toks)     # one pass over the layers for all
+    for i, (p, g, z) in enumerate(zip(prompts, toks, zs)):
         for s in range(len(g)):
             top = int(np.argmax(z[s]))
             steps += 1
@@ -187,3 +187,30 @@ def test_serve_level_profiles():
     p = st["level_seconds"][:3]
     assert p[0] > p[1] > p[2] > 0
     dm.close()
+
+
+def test_serve_7b_tokens_match_the_oracle():
+    """Llama-2-7B shape, requests drawn with the benchmark's recipe arriving over the first iterations,
+    at most 8 in flight, so requests are admitted into slots freed mid-run: the served tokens of a
+    request admitted at once, of two admitted late and of the longest prompt are the oracle's greedy
+    tokens (teacher-forced), up to provable near-ties."""
+    from paper_2403_12900_amd.binding import DecodeModel
+    cfg = CONFIGS["c3"]
+    wl = make_workload(cfg)
+    n = 20
+    prompts = [wl.tokens[i] for i in range(n)]
+    stops = [int(min(wl.stop_lens[i], 40)) for i in range(n)]
+    arrivals = [2 * i for i in range(n)]
+    max_ctx = max(len(p) + s - 1 for p, s in zip(prompts, stops))
+    need = sorted(((len(p) + s - 1 + 15) // 16 for p, s in zip(prompts, stops)), reverse=True)
+    say(f"serve 7B against the oracle: {n} requests, max_active 8, arrivals every 2 iterations")
+    dm = DecodeModel(cfg.model, cfg.weight_seed, max_slots=8, max_ctx=max_ctx, kv_blocks=sum(need[:8]))
+    toks, st = dm.serve(prompts, stops, max_active=8, arrivals=arrivals)
+    say("7B serve", st)
+    dm.close()
+    assert [len(t) for t in toks] == stops and st["max_batch"] <= 8
+    pick = sorted({0, 12, n - 1, int(np.argmax([len(p) for p in prompts]))})
+    w = R.Weights(oracle_shape(cfg.model), cfg.weight_seed, resident=False)
+    ties, steps = check_tokens_against_oracle(w, [prompts[i] for i in pick], [toks[i] for i in pick], 5e-2)
+    say("7B serve", f"requests {pick}: {steps} tokens, {ties} near-ties")
+    assert steps == sum(stops[i] for i in pick) and ties <= max(1, steps // 20)
