@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "decode tokens/s + achieved HBM GB/s, Llama-2-7B-shape bf16, ragged batch 32"
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
-DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16>, 2, 8, true>"
+DOMINANT = "k_stream_gemm<BF16, 1, 1, EpiSwiGLU<BF16>, 2, 8, true, true>"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_gemm_pmc_llama2_7b_b8.txt")
 
 
@@ -362,7 +362,9 @@ def time_prefill(model, m, wl, stops, reps: int = 3):
     re-run on freed slots.  Algorithmic flops: 2 x weight elements of the layer
     stack per prompt token, 4 x hd x H x (positions attended) per token and layer
     for attention, and the LM head for each prompt's last row; bf16 models issue
-    twice the projection MFMA work (hi + lo activation parts)."""
+    twice that MFMA work (hi + lo activation parts), and three times it for the
+    QKV projection (hi + mid + lo: its keys and values are rounded into the bf16
+    cache)."""
     import torch
     B = wl.batch
     tokens = int(sum(len(t) for t in wl.tokens))
@@ -380,12 +382,14 @@ def time_prefill(model, m, wl, stops, reps: int = 3):
         times.append(time.perf_counter() - t0)
     ms = 1e3 * min(times[1:])
     tflops = flops / (ms * 1e-3) / 1e12
-    issue = 2.0 if m.bf16 else 1.0
+    qkv_flops = 2.0 * tokens * m.n_layers * m.d_model * (m.n_heads + 2 * m.n_kv_heads) * m.head_dim
+    issue = (2.0 * flops + qkv_flops) / flops if m.bf16 else 1.0
     # mfma_frac counts the method's own 2 M N K flops; the MFMA work actually issued is `issued_factor`
-    # times that (bf16 activations go in as hi + lo parts), reported separately.
+    # times that (bf16 activations go in as hi + lo parts, the QKV input as hi + mid + lo), reported
+    # separately.
     return {"tokens": tokens, "ms": round(ms, 2), "tokens_per_s": round(tokens / (ms * 1e-3), 1),
             "algorithmic_tflops": round(tflops, 1), "peak_tflops": PEAK_BF16_TFLOPS,
-            "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4), "issued_factor": issue,
+            "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4), "issued_factor": round(issue, 3),
             "mfma_issued_tflops": round(tflops * issue, 1),
             "mfma_issued_frac": round(tflops * issue / PEAK_BF16_TFLOPS, 4)}
 

@@ -42,25 +42,17 @@ struct BF16 {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                    acc, 0, 0, 0);
   }
-  // Sum of squares of the activation values hi + lo of one fragment.
-  static __device__ __forceinline__ float sumsq(uint4 h, uint4 l) {
-    float s = 0.f;
-    const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
-    const uint32_t lw[4] = {l.x, l.y, l.z, l.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float v0 = __uint_as_float(hw[i] << 16) + __uint_as_float(lw[i] << 16);
-      const float v1 = __uint_as_float(hw[i] & 0xFFFF0000u) + __uint_as_float(lw[i] & 0xFFFF0000u);
-      s = fmaf(v0, v0, s);
-      s = fmaf(v1, v1, s);
-    }
-    return s;
-  }
-  // The hi and lo parts of an activation value.
-  static __device__ __forceinline__ void split(float v, elem* hi, elem* lo) {
-    *hi = from_f32(v);
-    *lo = from_f32(v - to_f32(*hi));
-  }
+};
+
+// bf16 weights whose activations come in three bf16 parts, hi = bf16(v),
+// mid = bf16(v - hi) and lo = bf16(v - hi - mid): every significant bit of
+// the fp32 activation (three MFMAs per fragment).  The QKV projection takes
+// its input this way because its keys and values are rounded into a bf16
+// cache, where an input error becomes a whole bf16 step of the elements it
+// moves across a rounding boundary; with 16-bit inputs those steps, not the
+// fp32 arithmetic, would set the distance to exact arithmetic.
+struct BF16x3 : BF16 {
+  static constexpr int parts = 3;
 };
 
 // fp32 storage: 16 elements per K-block, four MFMA 16x16x4 per fragment pair.
@@ -79,19 +71,10 @@ struct F32 {
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
     return acc;
   }
-  static __device__ __forceinline__ float sumsq(uint4 v, uint4) {
-    float s = 0.f;
-    s = fmaf(__uint_as_float(v.x), __uint_as_float(v.x), s);
-    s = fmaf(__uint_as_float(v.y), __uint_as_float(v.y), s);
-    s = fmaf(__uint_as_float(v.z), __uint_as_float(v.z), s);
-    s = fmaf(__uint_as_float(v.w), __uint_as_float(v.w), s);
-    return s;
-  }
-  static __device__ __forceinline__ void split(float v, elem* hi, elem*) { *hi = v; }
 };
 
 // Activation buffers (the MFMA B operand of the next projection) are
-// K-block-major: K-block kb of part q (hi / lo) of row b is a 64-byte run at
+// K-block-major: K-block kb of part q (hi, then mid / lo) of row b is a 64-byte run at
 // element offset ((kb * parts + q) * Rp + b) * kblk, Rp = padded rows.  The
 // 16 rows of one part of one K-block are therefore 1 KiB of consecutive
 // bytes, which is exactly what one 16-byte-per-lane load of a wave reads.
@@ -127,12 +110,18 @@ __device__ __forceinline__ int vtile_offset(int t, int dd) {
   }
 }
 
+// Stores activation value v of row b, feature k as its P::parts parts: each
+// part is the storage rounding of what the earlier parts leave (exact fp32
+// differences).
 template <class P>
 __device__ __forceinline__ void act_store(typename P::elem* act, int Rp, int b, int k, float v) {
-  typename P::elem hi, lo;
-  P::split(v, &hi, &lo);
-  act[act_offset<P>(Rp, b, k, 0)] = hi;
-  if constexpr (P::parts == 2) act[act_offset<P>(Rp, b, k, 1)] = lo;
+  float r = v;
+#pragma unroll
+  for (int q = 0; q < P::parts; ++q) {
+    const typename P::elem e = P::from_f32(r);
+    act[act_offset<P>(Rp, b, k, q)] = e;
+    r -= P::to_f32(e);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -15,7 +15,9 @@
 //   * a work-group may own RT row tiles, so each activation fragment feeds RT
 //     weight fragments (fewer activation bytes per weight byte);
 //   * bf16 activations come as hi + lo parts (two MFMAs per fragment), which
-//     keeps the activation side of every product near fp32 precision;
+//     keeps the activation side of every product near fp32 precision; the
+//     QKV projection's input comes as hi + mid + lo (all 24 bits, three
+//     MFMAs), since its keys and values are rounded into a bf16 cache;
 //   * per-wave accumulators are summed through LDS in a fixed order, so the
 //     result is bitwise reproducible.
 // RMSNorm (unit gains) of the input is fused: the sum of squares of each row
@@ -39,7 +41,7 @@ struct RowSlotPos {
 // (row tiles x activation tiles x parts): more in flight when registers allow.
 template <int XW>
 struct StreamDepth {
-  static constexpr int value = XW <= 2 ? 8 : XW <= 4 ? 4 : 2;
+  static constexpr int value = XW <= 3 ? 8 : XW <= 6 ? 4 : 2;
 };
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -56,23 +58,34 @@ __device__ __forceinline__ uint4 load_weight(const uint4* p) {
   }
 }
 
+// Activation fragments per K-block and 16-row tile: one per part, or, with
+// packed rows (PK: at most 8 rows, JT = 1), two parts per fragment -- lanes
+// of columns 0-7 carry part 2f of rows 0-7 and lanes of columns 8-15 part
+// 2f + 1 of the same rows, so a batch of at most 8 rows spends half the MFMA
+// columns and activation loads of the unpacked form.
+template <class P, bool PK>
+struct StreamFrags {
+  static constexpr int value = PK ? (P::parts + 1) / 2 : P::parts;
+};
+
 // One work-group computes RT consecutive 16-row output tiles for all rows;
 // its WAVES waves split the K-blocks, and each activation fragment a wave
 // loads feeds RT weight fragments.
-template <class P, int JT, int RT, int UH>
+template <int JT, int RT, int UH, int XF>
 struct StreamStage {
   uint4 a[UH][RT];                 // weight fragments
-  uint4 x[UH][JT][P::parts];       // activation fragments
+  uint4 x[UH][JT][XF];             // activation fragments
 };
 
-// Diagonal of the Gram accumulator g = X^T X of one 16-row activation tile,
-// i.e. the row's sum of squares, for the row of this lane's column.  The
-// diagonal entry of column c sits in lane c + 16 * (c / 4), register c % 4.
-__device__ __forceinline__ float gram_diagonal(const f32x4_t& gm, int lane) {
-  const int c = lane & 15;
-  const float cand = (c & 3) == 0 ? gm[0] : (c & 3) == 1 ? gm[1] : (c & 3) == 2 ? gm[2] : gm[3];
-  return __shfl(cand, c + 16 * (c >> 2));
+// Gram accumulator entries.  Entry (i, j) of a 16 x 16 MFMA accumulator sits
+// in lane j + 16 * (i / 4), register i % 4.  gram_pick(g, lane) is the
+// register each lane offers, g[lane % 4]; gram_entry(pick, i, j) then reads
+// entry (i, j) for any i = j (mod 4), in particular the diagonal.
+__device__ __forceinline__ float gram_pick(const f32x4_t& gm, int lane) {
+  const int r = lane & 3;
+  return r == 0 ? gm[0] : r == 1 ? gm[1] : r == 2 ? gm[2] : gm[3];
 }
+__device__ __forceinline__ float gram_entry(float pick, int i, int j) { return __shfl(pick, j + 16 * (i >> 2)); }
 
 // One work-group computes RT consecutive 16-row output tiles for all rows;
 // its WAVES waves split the K-blocks, and each activation fragment a wave
@@ -83,7 +96,14 @@ __device__ __forceinline__ float gram_diagonal(const f32x4_t& gm, int lane) {
 // X^T X of each activation fragment with itself has them on its diagonal.
 // For bf16 activations (x = hi + lo) that is hi.hi + 2 hi.lo, two MFMAs: the
 // diagonal of hi.lo equals that of lo.hi, and lo.lo (at most 2^-18 of the
-// sum) is left out.
+// sum) is left out.  With three parts (x = hi + mid + lo) it is hi.hi +
+// 2 hi.mid + mid.mid + 2 hi.lo, four MFMAs; the terms left out (mid.lo,
+// lo.lo) are at most 2^-24 of the sum.  Packed rows need fewer: the Gram
+// product of the fragment (hi | lo) with itself holds hi.hi on its diagonal
+// and hi.lo at (c, c + 8); that of (hi | mid) also holds mid.mid at (c + 8,
+// c + 8), and (hi | mid) times (lo | 0) gives hi.lo on the diagonal.  The
+// products themselves leave part 0 (and 2) of row c in accumulator column c
+// and part 1 in column c + 8, which the epilogue adds.
 // LDS floats the cross-wave reduction of stream_gemm_tiles needs.
 template <int JT, int WAVES, int RT>
 struct StreamRed {
@@ -91,43 +111,65 @@ struct StreamRed {
 };
 
 // The two pipeline stages of a wave's stream (U K-blocks in flight).
-template <class P, int JT, int RT, int U>
-using StreamStageOf = StreamStage<P, JT, RT, (U / 2 > 0 ? U / 2 : 1)>;
+template <class P, int JT, int RT, int U, bool PK>
+using StreamStageOf = StreamStage<JT, RT, (U / 2 > 0 ? U / 2 : 1), StreamFrags<P, PK>::value>;
 
 // The body of k_stream_gemm as a device function: the WAVES waves of the
 // calling work-group compute row tiles nt0 .. nt0 + RT - 1; red is LDS of
 // StreamRed<JT, WAVES, RT>::floats floats.  With WAVES > 1 every wave of the
 // work-group must call it (it synchronises the work-group).  s0, s1 are the
-// pipeline stages.
-template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream>
+// pipeline stages.  PK: packed rows (n_rows <= 8, JT = 1, two or three parts).
+// LP: parts per K-block of the activation record (at least P::parts; the
+// first P::parts are used).
+template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream, bool PK, int LP = P::parts>
 __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, const uint4* __restrict__ X, int KB,
                                                   int Rp, int n_rows, const Epi& epi, int nt0, int wave, int lane,
-                                                  float* red, StreamStageOf<P, JT, RT, U>& s0,
-                                                  StreamStageOf<P, JT, RT, U>& s1) {
+                                                  float* red, StreamStageOf<P, JT, RT, U, PK>& s0,
+                                                  StreamStageOf<P, JT, RT, U, PK>& s1) {
   constexpr int PARTS = P::parts;
+  static_assert(!PK || (JT == 1 && PARTS >= 2), "packed rows: one tile of at most 8 rows, two or three parts");
+  static_assert(LP >= PARTS, "the record holds the parts used");
+  constexpr int XF = StreamFrags<P, PK>::value;
   constexpr int UH = U / 2 > 0 ? U / 2 : 1;
-  using Stage = StreamStageOf<P, JT, RT, U>;
+  using Stage = StreamStageOf<P, JT, RT, U, PK>;
   const int kb0 = (KB * wave) / WAVES, kb1 = (KB * (wave + 1)) / WAVES;
-  f32x4_t acc[RT][JT], gram[JT], gram_hl[JT];
+  // Gram accumulators per activation tile: hi.hi, then hi.lo (two parts) or
+  // hi.mid, mid.mid, hi.lo (three parts); packed: (hi|lo)^2, or (hi|mid)^2
+  // and (hi|mid).(lo|0).
+  constexpr int NG = PK ? XF : PARTS == 3 ? 4 : PARTS;
+  f32x4_t acc[RT][JT], gram[JT][NG];
 #pragma unroll
   for (int j = 0; j < JT; ++j) {
 #pragma unroll
     for (int t = 0; t < RT; ++t) acc[t][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    gram[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    gram_hl[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NG; ++i) gram[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   const uint4* wp = W + static_cast<size_t>(nt0) * KB * 64 + lane;
   const size_t wtile = static_cast<size_t>(KB) * 64;  // uint4 per row tile
-  // Lanes of rows past n_rows read row 0 instead (the same cache lines as a
-  // valid lane, so no extra traffic); their accumulator columns are never
-  // stored, and MFMA columns do not mix, so the values they read do not matter.
+  // This lane's uint4 offset within a K-block's activation record; fragment f
+  // adds f * xstep.  Lanes of rows past n_rows read row 0 instead (the same
+  // cache lines as a valid lane, so no extra traffic); their accumulator
+  // columns are never stored, and MFMA columns do not mix, so the values they
+  // read do not matter.  Packed: lane column c reads part 2 f + c / 8 of row
+  // c % 8; for three parts, columns 8-15 of fragment 1 (part 3: the next
+  // K-block's part 0, or past the last K-block's record, inside the buffer)
+  // are zeroed after the load.
+  const int xpart = Rp * 4;                  // uint4 per (K-block, part)
+  const int xstep = PK ? 2 * xpart : xpart;  // uint4 between a lane's fragments
   int xoff[JT];
 #pragma unroll
   for (int j = 0; j < JT; ++j) {
-    const int b = 16 * j + (lane & 15);
-    xoff[j] = (b < n_rows ? b : 0) * 4 + (lane >> 4);
+    if constexpr (PK) {
+      const int c = lane & 15, r = c & 7;
+      xoff[j] = (c >> 3) * xpart + (r < n_rows ? r : 0) * 4 + (lane >> 4);
+    } else {
+      const int b = 16 * j + (lane & 15);
+      xoff[j] = (b < n_rows ? b : 0) * 4 + (lane >> 4);
+    }
   }
-  const size_t xpart = static_cast<size_t>(Rp) * 4;  // uint4 per (K-block, part)
+  const bool zero_hi = PK && PARTS == 3 && (lane & 15) >= 8;  // packed (lo | 0): columns 8-15 are zero
+  const size_t xblk = static_cast<size_t>(LP) * xpart;        // uint4 per K-block
   // Operands the epilogue reads from memory (residual, rotary table, block
   // table) are fetched now, by the wave that runs the epilogue, so their
   // latency hides under the weight stream instead of ending the kernel.
@@ -137,32 +179,51 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
     for (int t = 0; t < RT; ++t) pre[t] = epi.template prefetch<JT>(nt0 + t, lane);
   }
 
-  auto load = [&](Stage& st, int kb) {
+  auto load1 = [&](Stage& st, int u, int kb) {
 #pragma unroll
-    for (int u = 0; u < UH; ++u) {
+    for (int t = 0; t < RT; ++t) st.a[u][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb) * 64);
 #pragma unroll
-      for (int t = 0; t < RT; ++t) st.a[u][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb + u) * 64);
+    for (int j = 0; j < JT; ++j)
 #pragma unroll
-      for (int j = 0; j < JT; ++j)
-#pragma unroll
-        for (int q = 0; q < PARTS; ++q) st.x[u][j][q] = X[(static_cast<size_t>(kb + u) * PARTS + q) * xpart + xoff[j]];
-    }
+      for (int f = 0; f < XF; ++f) st.x[u][j][f] = X[static_cast<size_t>(kb) * xblk + f * xstep + xoff[j]];
   };
-  auto compute = [&](const Stage& st) {
+  auto compute1 = [&](const Stage& st, int u) {
 #pragma unroll
-    for (int u = 0; u < UH; ++u) {
+    for (int j = 0; j < JT; ++j) {
+      uint4 x[XF];
 #pragma unroll
-      for (int j = 0; j < JT; ++j) {
+      for (int f = 0; f < XF; ++f) x[f] = st.x[u][j][f];
+      if constexpr (PK && PARTS == 3) {
+        x[1].x = zero_hi ? 0u : x[1].x;
+        x[1].y = zero_hi ? 0u : x[1].y;
+        x[1].z = zero_hi ? 0u : x[1].z;
+        x[1].w = zero_hi ? 0u : x[1].w;
+      }
 #pragma unroll
-        for (int t = 0; t < RT; ++t)
+      for (int t = 0; t < RT; ++t)
 #pragma unroll
-          for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[u][t], st.x[u][j][q]);
-        if constexpr (Epi::kNorm) {
-          gram[j] = P::mma(gram[j], st.x[u][j][0], st.x[u][j][0]);
-          if constexpr (PARTS == 2) gram_hl[j] = P::mma(gram_hl[j], st.x[u][j][0], st.x[u][j][1]);
+        for (int f = 0; f < XF; ++f) acc[t][j] = P::mma(acc[t][j], st.a[u][t], x[f]);
+      if constexpr (Epi::kNorm) {
+        gram[j][0] = P::mma(gram[j][0], x[0], x[0]);
+        if constexpr (PK) {
+          if constexpr (XF == 2) gram[j][1] = P::mma(gram[j][1], x[0], x[1]);
+        } else {
+          if constexpr (PARTS >= 2) gram[j][1] = P::mma(gram[j][1], x[0], x[1]);
+          if constexpr (PARTS == 3) {
+            gram[j][2] = P::mma(gram[j][2], x[1], x[1]);
+            gram[j][3] = P::mma(gram[j][3], x[0], x[2]);
+          }
         }
       }
     }
+  };
+  auto load = [&](Stage& st, int kb) {
+#pragma unroll
+    for (int u = 0; u < UH; ++u) load1(st, u, kb + u);
+  };
+  auto compute = [&](const Stage& st) {
+#pragma unroll
+    for (int u = 0; u < UH; ++u) compute1(st, u);
   };
 
   const int nstage = (kb1 - kb0) / UH;
@@ -176,30 +237,37 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
     }
   }
   for (int kb = kb0 + nstage * UH; kb < kb1; ++kb) {
-    Stage& st = s0;
-#pragma unroll
-    for (int t = 0; t < RT; ++t) st.a[0][t] = load_weight<kStream>(wp + t * wtile + static_cast<size_t>(kb) * 64);
-#pragma unroll
-    for (int j = 0; j < JT; ++j)
-#pragma unroll
-      for (int q = 0; q < PARTS; ++q) st.x[0][j][q] = X[(static_cast<size_t>(kb) * PARTS + q) * xpart + xoff[j]];
-#pragma unroll
-    for (int j = 0; j < JT; ++j) {
-#pragma unroll
-      for (int t = 0; t < RT; ++t)
-#pragma unroll
-        for (int q = 0; q < PARTS; ++q) acc[t][j] = P::mma(acc[t][j], st.a[0][t], st.x[0][j][q]);
-      if constexpr (Epi::kNorm) {
-        gram[j] = P::mma(gram[j], st.x[0][j][0], st.x[0][j][0]);
-        if constexpr (PARTS == 2) gram_hl[j] = P::mma(gram_hl[j], st.x[0][j][0], st.x[0][j][1]);
-      }
-    }
+    load1(s0, 0, kb);
+    compute1(s0, 0);
   }
   float ssq[JT];
 #pragma unroll
-  for (int j = 0; j < JT; ++j)
-    ssq[j] = Epi::kNorm ? gram_diagonal(gram[j], lane) + (PARTS == 2 ? 2.f * gram_diagonal(gram_hl[j], lane) : 0.f)
-                        : 0.f;
+  for (int j = 0; j < JT; ++j) {
+    ssq[j] = 0.f;
+    if constexpr (Epi::kNorm) {
+      if constexpr (PK) {
+        // Row c = lane column mod 8 (lanes of columns 8-15 compute row c's
+        // again, unused).
+        const int c = lane & 7;
+        const float p0 = gram_pick(gram[j][0], lane);
+        ssq[j] = gram_entry(p0, c, c);
+        if constexpr (XF == 1) {
+          ssq[j] += 2.f * gram_entry(p0, c, c + 8);
+        } else {
+          const float p1 = gram_pick(gram[j][1], lane);
+          ssq[j] += 2.f * (gram_entry(p0, c, c + 8) + gram_entry(p1, c, c)) + gram_entry(p0, c + 8, c + 8);
+        }
+      } else {
+        const int c = lane & 15;
+        ssq[j] = gram_entry(gram_pick(gram[j][0], lane), c, c);
+        if constexpr (PARTS == 2) ssq[j] += 2.f * gram_entry(gram_pick(gram[j][1], lane), c, c);
+        if constexpr (PARTS == 3)
+          ssq[j] += 2.f * (gram_entry(gram_pick(gram[j][1], lane), c, c) +
+                           gram_entry(gram_pick(gram[j][3], lane), c, c)) +
+                    gram_entry(gram_pick(gram[j][2], lane), c, c);
+      }
+    }
+  }
   if constexpr (WAVES > 1) {
     // red[w - 1][j][4 t + c][lane], then the sums of squares at [.][j][4 RT][lane].
     auto at = [&](int w, int j, int i) -> float& { return red[((w * JT + j) * (4 * RT + 1) + i) * 64 + lane]; };
@@ -226,19 +294,50 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
       }
     }
   }
+  if constexpr (PK) {
+    // Row c's parts 0 (and 2) are in column c, part 1 in column c + 8.
+    const int src = (lane & 48) | ((lane + 8) & 15);
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[t][0][c] += __shfl(acc[t][0][c], src);
+  }
 #pragma unroll
   for (int t = 0; t < RT; ++t) epi.template apply<JT>(nt0 + t, acc[t], ssq, lane, pre[t]);
 }
 
 template <class P, int JT, int WAVES, class Epi, int RT = 1, int U = StreamDepth<RT * JT * P::parts>::value,
-          bool kStream = false>
+          bool kStream = false, bool PK = false>
 __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X,
                                                             int KB, int Rp, int n_rows, Epi epi) {
   __shared__ float red[StreamRed<JT, WAVES, RT>::floats];
-  StreamStageOf<P, JT, RT, U> s0, s1;
-  stream_gemm_tiles<P, JT, WAVES, Epi, RT, U, kStream>(W, X, KB, Rp, n_rows, epi, blockIdx.x * RT,
-                                                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
-                                                       threadIdx.x & 63, red, s0, s1);
+  StreamStageOf<P, JT, RT, U, PK> s0, s1;
+  stream_gemm_tiles<P, JT, WAVES, Epi, RT, U, kStream, PK>(W, X, KB, Rp, n_rows, epi, blockIdx.x * RT,
+                                                           __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
+                                                           threadIdx.x & 63, red, s0, s1);
+}
+
+// QKV projection of bf16 models over a three-part record: query tiles (the
+// first q_tiles, a multiple of RT) take its first two parts -- hi and mid are
+// the two-part form of the same values -- and key and value tiles, which are
+// rounded into the bf16 cache, all three.  The branch is uniform per
+// work-group.
+template <int JT, int WAVES, class Epi, int RT, int U2, int U3, bool PK>
+__global__ __launch_bounds__(WAVES * 64) void k_stream_gemm_qkv(const uint4* __restrict__ W,
+                                                                const uint4* __restrict__ X, int KB, int Rp,
+                                                                int n_rows, Epi epi, int q_tiles) {
+  __shared__ float red[StreamRed<JT, WAVES, RT>::floats];
+  const int nt0 = blockIdx.x * RT;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (nt0 < q_tiles) {
+    StreamStageOf<BF16, JT, RT, U2, PK> s0, s1;
+    stream_gemm_tiles<BF16, JT, WAVES, Epi, RT, U2, true, PK, 3>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane, red,
+                                                                 s0, s1);
+  } else {
+    StreamStageOf<BF16x3, JT, RT, U3, PK> s0, s1;
+    stream_gemm_tiles<BF16x3, JT, WAVES, Epi, RT, U3, true, PK>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane, red,
+                                                                s0, s1);
+  }
 }
 
 // Stores four consecutive features n0..n0+3 of row b into an activation buffer.

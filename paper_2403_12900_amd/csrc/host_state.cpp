@@ -3,6 +3,7 @@
 
 #include <utility>
 
+#include <algorithm>
 #include <cmath>
 #include <limits>
 
@@ -104,8 +105,12 @@ Layout layout(const Dims& d) {
   l.off_bt = take(static_cast<size_t>(d.S) * d.mb * sizeof(int32_t));
   // Per-row buffers hold a whole prefill chunk (decode passes use the first rows).
   l.off_x = take(static_cast<size_t>(kPrefillRows) * d.d * sizeof(float));
-  // Activation records carry hi + lo parts for bf16 models.
-  l.act_bytes = static_cast<size_t>(d.kb_max) * kPrefillRows * d.kblk * d.esize * (d.dtype == SPR_BF16 ? 2 : 1);
+  // Activation records carry hi + lo parts for bf16 models, and the QKV
+  // input (d features) hi + mid + lo.
+  const size_t act_blocks = d.dtype == SPR_BF16
+                                ? std::max(2 * static_cast<size_t>(d.kb_max), 3 * static_cast<size_t>(d.kb_d))
+                                : static_cast<size_t>(d.kb_max);
+  l.act_bytes = act_blocks * kPrefillRows * d.kblk * d.esize;
   l.off_act0 = take(l.act_bytes);
   l.off_act1 = take(l.act_bytes);
   l.off_q = take(static_cast<size_t>(kPrefillRows) * d.H * d.hd * sizeof(float));

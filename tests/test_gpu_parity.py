@@ -316,16 +316,33 @@ def _shortest(ctx, n):
     return [int(i) for i in np.argsort(ctx, kind="stable")[:n]]
 
 
+def _longest(ctx, n):
+    return [int(i) for i in np.argsort(ctx, kind="stable")[::-1][:n]]
+
+
 def _nearest(ctx, target):
     return int(np.argmin(np.abs(ctx - target)))
 
 
+def _at_ranks(ctx, taken, quantiles):
+    """One request per quantile of the context lengths (the request at that rank of the sorted
+    contexts, or the next longer one not already in `taken`)."""
+    order = [int(i) for i in np.argsort(ctx, kind="stable")]
+    out = list(taken)
+    for q in quantiles:
+        r = int(round(q * (len(order) - 1)))
+        while order[r] in out:
+            r += 1
+        out.append(order[r])
+    return out
+
+
 def test_llama2_7b_ragged_batch32():
     """The benchmarked workload at full size: all 32 requests decode to their stop lengths.  Checked at
-    every step: the request with the longest context (616-token prompt, 1020 generated, 1635 positions
-    at its last step -- it decodes alone for half of the batch's steps), the one nearest the median
-    context, and the two shortest."""
-    _full_size("c3", lambda ctx: _shortest(ctx, 2) + [int(np.argmax(ctx)), _nearest(ctx, np.median(ctx))])
+    every step: the three longest contexts (1635, 1234 and 1107 positions at the last step; the
+    longest, a 616-token prompt with 1020 generated, decodes alone for half of the batch's steps), the
+    one nearest the median context (307) and the two shortest (132, 149): every directive level."""
+    _full_size("c3", lambda ctx: _shortest(ctx, 2) + _longest(ctx, 3) + [_nearest(ctx, np.median(ctx))])
 
 
 def test_llama2_7b_batch1_256_tokens():
@@ -334,13 +351,15 @@ def test_llama2_7b_batch1_256_tokens():
 
 
 def test_llama2_13b_ragged_batch64():
-    """13B shape, 64 ragged requests in 16-position KV pages: the longest context (1353 positions) and
-    the two shortest are checked at every step."""
-    _full_size("c4", lambda ctx: _shortest(ctx, 2) + [int(np.argmax(ctx))])
+    """13B shape, 64 ragged requests in 16-position KV pages, eight of them checked at every step: the
+    longest context (1353 positions), the two shortest (127, 144) and one at each of the 20th, 40th,
+    50th, 60th and 80th percentiles of the contexts (234 to 580 positions): every directive level."""
+    _full_size("c4", lambda ctx: _at_ranks(ctx, _shortest(ctx, 2) + _longest(ctx, 1), (0.2, 0.4, 0.5, 0.6, 0.8)))
 
 
 def test_llama2_70b_gqa_ragged_batch16():
     """70B shape with grouped-query attention (8 query heads per KV head), ~138 GB of weights on one
-    GPU: the request nearest the median context (884 positions) and the shortest are checked at every
-    step against the oracle, which streams the weights layer by layer."""
-    _full_size("c5", lambda ctx: _shortest(ctx, 1) + [_nearest(ctx, np.median(ctx))])
+    GPU: four requests, the one nearest the median context (884 positions) and the three shortest
+    (177, 292, 381), are checked at every step against the oracle, which streams the weights layer by
+    layer."""
+    _full_size("c5", lambda ctx: _shortest(ctx, 3) + [_nearest(ctx, np.median(ctx))])
