@@ -16,6 +16,8 @@ Runs (cache format / arithmetic of the cached values):
                 fp32 rotary embedding (what a fp32-accumulating device does),
                 rounded to bf16
   bf16_f64_ulp  the fp64 values moved up by one fp32 ulp, then rounded to bf16
+  bf16_hilo     as bf16_f32, but the projection input carried as two bf16
+                parts (hi = bf16(a), lo = bf16(a - hi): 16 significant bits)
   f32_f64       fp64 values rounded to fp32
   f32_f32       fp32 arithmetic as in bf16_f32, kept in fp32
 Everything else (norms, projections, attention, MLP, LM head) is the oracle's
@@ -30,7 +32,7 @@ import numpy as np
 
 from oracle import llama_ref as R
 
-RUNS = ("bf16_f64", "bf16_f32", "bf16_f64_ulp", "f32_f64", "f32_f32")
+RUNS = ("bf16_f64", "bf16_f32", "bf16_f64_ulp", "bf16_hilo", "f32_f64", "f32_f32")
 
 
 def _rope_f32(x32: np.ndarray, positions: Sequence[int], base: float) -> np.ndarray:
@@ -52,10 +54,17 @@ def _to_bf16(f32: np.ndarray) -> np.ndarray:
     return u.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
+def _hi_lo(a32: np.ndarray) -> np.ndarray:
+    """fp32 values as the sum of their two bf16 parts hi = bf16(a), lo = bf16(a - hi) (exact in fp32)."""
+    hi = _to_bf16(a32)
+    lo = _to_bf16((a32.astype(np.float64) - hi).astype(np.float32))
+    return (hi + lo).astype(np.float32)
+
+
 def _cached(run: str, kv64: np.ndarray, kv32: np.ndarray) -> np.ndarray:
     if run == "bf16_f64":
         return R.round_to_storage(kv64, bf16=True)
-    if run == "bf16_f32":
+    if run in ("bf16_f32", "bf16_hilo"):
         return _to_bf16(kv32)
     if run == "bf16_f64_ulp":
         return _to_bf16(np.nextafter(kv64.astype(np.float32), np.float32(np.inf)))
@@ -85,6 +94,9 @@ def lockstep_logits(shape: R.Shape, seed: int, tokens: Sequence[int], runs: Sequ
         k64 = (A @ W["wk"].T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         v64 = (A @ W["wv"].T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         A32 = A.astype(np.float32)
+        for i, r in enumerate(runs):
+            if r == "bf16_hilo":
+                A32[i * T:(i + 1) * T] = _hi_lo(A32[i * T:(i + 1) * T])
         k32 = (A32 @ W["wk"].astype(np.float32).T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         v32 = (A32 @ W["wv"].astype(np.float32).T).reshape(nr, T, sh.n_kv_heads, sh.head_dim)
         O = np.empty((nr, T, sh.n_heads * sh.head_dim))
@@ -108,11 +120,13 @@ def lockstep_logits(shape: R.Shape, seed: int, tokens: Sequence[int], runs: Sequ
 
 def floors(z: Dict[str, np.ndarray]) -> Dict[str, Dict[str, float]]:
     """Worst (over positions) max-abs and relative-L2 logit differences between the runs that share
-    a cache format."""
+    a cache format, and the mean over positions of each position's relative L2 difference."""
     out = {}
-    for a, b in (("bf16_f64", "bf16_f32"), ("bf16_f64", "bf16_f64_ulp"), ("f32_f64", "f32_f32")):
+    for a, b in (("bf16_f64", "bf16_f32"), ("bf16_f64", "bf16_f64_ulp"), ("bf16_f64", "bf16_hilo"),
+                 ("f32_f64", "f32_f32")):
         if a in z and b in z:
             d = z[a] - z[b]
-            out[f"{a}~{b}"] = {"max_abs": float(np.abs(d).max()),
-                               "rel_l2": float((np.linalg.norm(d, axis=1) / np.linalg.norm(z[a], axis=1)).max())}
+            rel = np.linalg.norm(d, axis=1) / np.linalg.norm(z[a], axis=1)
+            out[f"{a}~{b}"] = {"max_abs": float(np.abs(d).max()), "rel_l2": float(rel.max()),
+                               "mean_rel_l2": float(rel.mean())}
     return out
