@@ -121,10 +121,12 @@ struct TileShape {
   static_assert(GN * GM == NW && WN * GN == TN && WM * GM == TM, "tile shape");
 };
 
-template <class P, int TN, int TM, class Epi, int NW = 4>
+// LP: parts per K-block of the activation record (the first P::parts are used).
+template <class P, int TN, int TM, class Epi, int NW = 4, int LP = P::parts>
 __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__ W, const uint4* __restrict__ X,
                                                        int NT, int KB, int Rp, Epi epi) {
   constexpr int PARTS = P::parts;
+  static_assert(LP >= PARTS, "the record holds the parts used");
   constexpr int NFRAG = TN + TM * PARTS;
   static_assert(NFRAG % NW == 0, "fragments per stage must split over the waves");
   constexpr int L = NFRAG / NW;  // loads per wave per stage
@@ -167,7 +169,7 @@ __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__
       } else {
         const int a = f - TN, q = a / TM, tt = a % TM;
         const int r0 = min(m0 + 16 * tt, Rp - 16);
-        src = X + (static_cast<size_t>(kb) * PARTS + q) * xpart + static_cast<size_t>(r0) * 4 + xlane;
+        src = X + (static_cast<size_t>(kb) * LP + q) * xpart + static_cast<size_t>(r0) * 4 + xlane;
       }
       __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)&dst[f][0], 16, 0, 0);
     }
@@ -233,6 +235,7 @@ __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__
 template <class P, class KP = P>
 struct EpiQKVRows {
   int M, H, Hkv, hd, mb;
+  int nt_base;                    // weight tile of the launch's tile 0 (the launch may cover part of QKV)
   float* q;                       // [rows][H * hd]
   typename KP::elem* kc;
   typename KP::elem* vc;
@@ -244,7 +247,7 @@ struct EpiQKVRows {
   __device__ __forceinline__ void apply_tile(int nt, int m0, const f32x4_t& acc, int lane) const {
     const int b = m0 + (lane & 15);
     if (b >= M) return;
-    const int n0 = 16 * nt + 4 * (lane >> 4);
+    const int n0 = 16 * (nt_base + nt) + 4 * (lane >> 4);
     const int qr = H * hd, kr = Hkv * hd;
     const float s = rs[b];
     float v0 = acc[0] * s, v1 = acc[1] * s, v2 = acc[2] * s, v3 = acc[3] * s;

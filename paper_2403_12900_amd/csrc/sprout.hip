@@ -582,28 +582,30 @@ void launch_attn_prefill(spr_model* m, int layer, const PrefillChunk& ch, int Rp
 // else 64 features x 128 rows, else 64 x 64.
 // Three-part activations (QKV) take 256 features x 128 rows instead of 256 x
 // 256: the larger tile's three LDS stages would need 192 KiB.
-template <class P, class Epi>
+// LP: parts per K-block of the activation record X (P::parts used).
+template <class P, class Epi, int LP = P::parts>
 void launch_tile_gemm(hipStream_t st, const char* W, const char* X, int NT, int KB, int Rp, const Epi& e) {
   const uint4* w = reinterpret_cast<const uint4*>(W);
   const uint4* x = reinterpret_cast<const uint4*>(X);
   const int mt = Rp / 128;
   if constexpr (P::parts == 3) {
     if (ceil_div(NT, 16) * mt >= 256) {
-      k_tile_gemm<P, 16, 8, Epi, 8><<<dim3(ceil_div(NT, 16), mt), 512, 0, st>>>(w, x, NT, KB, Rp, e);
+      k_tile_gemm<P, 16, 8, Epi, 8, LP><<<dim3(ceil_div(NT, 16), mt), 512, 0, st>>>(w, x, NT, KB, Rp, e);
       return;
     }
   } else {
     if (ceil_div(NT, 16) * ceil_div(Rp, 256) >= 256) {
-      k_tile_gemm<P, 16, 16, Epi, 8><<<dim3(ceil_div(NT, 16), ceil_div(Rp, 256)), 512, 0, st>>>(w, x, NT, KB, Rp, e);
+      k_tile_gemm<P, 16, 16, Epi, 8, LP><<<dim3(ceil_div(NT, 16), ceil_div(Rp, 256)), 512, 0, st>>>(w, x, NT, KB, Rp,
+                                                                                                    e);
       return;
     }
   }
   if (ceil_div(NT, 8) * mt >= 512) {
-    k_tile_gemm<P, 8, 8, Epi><<<dim3(ceil_div(NT, 8), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+    k_tile_gemm<P, 8, 8, Epi, 4, LP><<<dim3(ceil_div(NT, 8), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
   } else if (ceil_div(NT, 4) * mt >= 512) {
-    k_tile_gemm<P, 4, 8, Epi><<<dim3(ceil_div(NT, 4), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+    k_tile_gemm<P, 4, 8, Epi, 4, LP><<<dim3(ceil_div(NT, 4), mt), 256, 0, st>>>(w, x, NT, KB, Rp, e);
   } else {
-    k_tile_gemm<P, 4, 4, Epi><<<dim3(ceil_div(NT, 4), Rp / 64), 256, 0, st>>>(w, x, NT, KB, Rp, e);
+    k_tile_gemm<P, 4, 4, Epi, 4, LP><<<dim3(ceil_div(NT, 4), Rp / 64), 256, 0, st>>>(w, x, NT, KB, Rp, e);
   }
 }
 
@@ -634,7 +636,18 @@ spr_status prefill_pass(spr_model* m, const PrefillChunk& ch, int32_t* tok, floa
       e.rope = p.rope();
       e.rows = p.prow();
       e.rs = p.rs();
-      launch_tile_gemm<QKVIn<P>>(m->st, p.wqkv(l), p.act(0), d.nt_qkv, d.kb_d, Rp, e);
+      e.nt_base = 0;
+      if constexpr (QKVIn<P>::parts == 3) {
+        // Query tiles take hi + mid of the three-part record (and the larger
+        // two-part tiles), key and value tiles all three parts.
+        const int q_tiles = d.H * d.hd / 16;
+        launch_tile_gemm<P, EpiQKVRows<P, KP>, 3>(m->st, p.wqkv(l), p.act(0), q_tiles, d.kb_d, Rp, e);
+        e.nt_base = q_tiles;
+        const char* wkv = p.wqkv(l) + static_cast<size_t>(q_tiles) * d.kb_d * 64 * sizeof(uint4);
+        launch_tile_gemm<QKVIn<P>>(m->st, wkv, p.act(0), d.nt_qkv - q_tiles, d.kb_d, Rp, e);
+      } else {
+        launch_tile_gemm<QKVIn<P>>(m->st, p.wqkv(l), p.act(0), d.nt_qkv, d.kb_d, Rp, e);
+      }
     }
     if (d.hd == 128) {
       launch_attn_prefill<P, KP, 128>(m, l, ch, Rp);
