@@ -271,6 +271,27 @@ def test_rewind_regenerates_identically():
     dm.close()
 
 
+@pytest.mark.parametrize("case", ["bf16_gqa4_hd128_wide_o", "bf16_gqa4_hd128_long_context"])
+def test_repeat_runs_are_bitwise_identical(case):
+    """Two runs of the same batch give bitwise equal tokens and logits at every step: cross-wave and
+    cross-split reductions have a fixed order (the split merge counts arrivals with an atomic, but the
+    last split reads every partial in split order).  The first case passes through 20, 15 and 5 rows
+    (two-tile, one-tile and packed-row projections), the second through attention splits over a
+    1690-position context."""
+    m, plens, stops = TOY_CASES[case]
+    say(f"repeat runs {case}")
+    rng = np.random.default_rng(11)
+    prompts = _prompts(rng, m.vocab, plens)
+    a = DeviceRun(m, 80, prompts, stops)
+    b = DeviceRun(m, 80, prompts, stops)
+    for i in range(len(prompts)):
+        assert a.tokens[i] == b.tokens[i], (case, i)
+        for s_, z in a.logits[i].items():
+            assert np.array_equal(z.view(np.uint32), b.logits[i][s_].view(np.uint32)), (case, i, s_)
+    a.close()
+    b.close()
+
+
 def test_batch_invariance():
     """A request decoded alone or inside a batch gives the same tokens and logits within tolerance."""
     m, plens, stops = TOY_CASES["bf16_gqa4_hd128_wide_o"]
