@@ -4,18 +4,19 @@
 //
 // A decode step (one token row per active request) enqueues on the model's
 // stream:
-//   k_embed                      token rows -> fp32 residual x, activation
+//   k_embed                      token rows -> fp32 residual x, QKV input (three parts)
 //   per layer:
-//     k_stream_gemm<EpiQKV>      RMSNorm . Wqkv, RoPE, q out, k/v appended to the paged cache
+//     k_stream_gemm_qkv<EpiQKV>  RMSNorm . Wqkv, RoPE, q out, k/v appended to the paged cache
 //     k_attn_decode (+merge)     softmax(q K^T / sqrt(hd)) V over the row's cached positions
 //     k_stream_gemm<EpiResid>    x += o Wo^T
 //     k_stream_gemm<EpiSwiGLU>   h = SiLU(RMSNorm(x) W1^T) * (RMSNorm(x) W3^T)
-//     k_stream_gemm<EpiResid>    x += h W2^T
+//     k_stream_gemm<EpiResid>    x += h W2^T (and the next QKV input)
 //   k_stream_gemm<EpiLogits>     RMSNorm(x) Wlm^T, per-tile greedy candidates
 //   k_argmax_final               tok[slot] = lowest index of the row maximum
-// A prefill chunk (up to 1024 prompt rows of one or more requests) runs the
+// A prefill chunk (up to 4096 prompt rows of one or more requests) runs the
 // same layer stack on tiled, compute-bound kernels:
-//   k_embed_rows; per layer k_row_rscale, k_tile_gemm<EpiQKVRows>,
+//   k_embed_rows; per layer k_row_rscale, k_tile_gemm<EpiQKVRows> (query
+//   tiles, then key and value tiles),
 //   k_attn_prefill (causal, 16 queries per MFMA), k_tile_gemm<EpiResidRows>,
 //   k_row_rscale, k_tile_gemm<EpiSwiGLURows>, k_tile_gemm<EpiResidRows>;
 //   then k_gather_rows of the rows that end a prompt, and the decode LM head.
