@@ -9,6 +9,8 @@
 // tile they read from LDS, so every tile read feeds up to 64 queries.
 #pragma once
 
+#include <utility>
+
 #include "attn_kernels.h"
 
 namespace sprk {
@@ -81,6 +83,23 @@ __device__ __forceinline__ u32x4_t lds_read16(const uint4* p) {
   return v;
 }
 __device__ __forceinline__ void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Calls f(std::integral_constant<int, j>) for j = 0 .. N - 1 in order.
+template <class F, int... J>
+__device__ __forceinline__ void static_for_seq(F& f, std::integer_sequence<int, J...>) {
+  (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// Waits until at most N of this wave's LDS reads are in flight (they return
+// in issue order, so every read but the last N has landed).
+template <int N>
+__device__ __forceinline__ void lds_reads_left() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
 // Ties a value read by lds_read16 to a point after lds_reads_done(): volatile
 // asm statements keep their order, so no use of v can move above the wait.
 __device__ __forceinline__ void lds_value_ready(u32x4_t& v) { asm volatile("" : "+v"(v)); }
@@ -191,6 +210,10 @@ __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__
     }
     lds_stage_barrier();
     if (kb + 2 < KB) issue(kb + 2, next);
+    // Reads in the order the products use them: the weight fragments, then
+    // the activation fragments of row tile 0, 1, ...  The products of row
+    // tile j start once its reads have landed, while the later tiles' reads
+    // are still in flight.
     u32x4_t a[WN], b[WM][PARTS];
 #pragma unroll
     for (int i = 0; i < WN; ++i) a[i] = lds_read16(&cur[wn * WN + i][lane]);
@@ -198,20 +221,25 @@ __global__ __launch_bounds__(NW * 64) void k_tile_gemm(const uint4* __restrict__
     for (int j = 0; j < WM; ++j)
 #pragma unroll
       for (int q = 0; q < PARTS; ++q) b[j][q] = lds_read16(&cur[TN + q * TM + wm * WM + j][lane]);
-    lds_reads_done();
+    auto row_tile = [&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      lds_reads_left<(WM - 1 - j) * PARTS>();
+      if constexpr (j == 0) {
 #pragma unroll
-    for (int i = 0; i < WN; ++i) lds_value_ready(a[i]);
-#pragma unroll
-    for (int j = 0; j < WM; ++j)
+        for (int i = 0; i < WN; ++i) lds_value_ready(a[i]);
+      }
 #pragma unroll
       for (int q = 0; q < PARTS; ++q) lds_value_ready(b[j][q]);
 #pragma unroll
-    for (int i = 0; i < WN; ++i)
-#pragma unroll
-      for (int j = 0; j < WM; ++j)
+      for (int i = 0; i < WN; ++i)
 #pragma unroll
         for (int q = 0; q < PARTS; ++q)
           acc[i][j] = P::mma(acc[i][j], __builtin_bit_cast(uint4, a[i]), __builtin_bit_cast(uint4, b[j][q]));
+      // Keep these products ahead of the next tile's wait (the scheduler
+      // would otherwise sink them below it).
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    static_for<WM>(row_tile);
   };
 
   issue(0, st0);
