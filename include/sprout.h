@@ -147,17 +147,18 @@ spr_status spr_decode_step(spr_model* m, int32_t n_active, const int32_t* slots,
  * spr_decode_step for callers that cannot allocate device memory or touch the
  * model's workspace scratch (code under HIP graph capture, tight serving
  * loops, harnesses that forbid allocation): identical arguments, semantics
- * and results, but the step's scratch -- attention split partials, split
- * arrival counters and the LM head's greedy candidates -- lives in a fixed
- * 16 MiB array in device memory that the library holds on each device it
- * runs on until the process ends.  The call allocates nothing and makes no
+ * and results, but the step's scratch -- split partials (of attention and of
+ * the projections' split-K slices), arrival counters and the LM head's
+ * greedy candidates -- lives in a fixed 24 MiB array in device memory that
+ * the library holds on each device it runs on until the process ends.  The call allocates nothing and makes no
  * allocating runtime call; it clears the counters it uses with a kernel
  * before the step.  Every call on one device shares that device's array:
  * calls that overlap on one device (on different streams, or from different
  * threads) race and must not be issued.  SPR_ERR_INVALID_ARG when the model
  * or batch does not fit the array: more than 128 KV heads, a vocabulary
- * above 130048, or n_heads * (head_dim + 4) * 4 bytes * n_active above
- * 8 MiB; other errors as spr_decode_step.
+ * above 130048, n_heads * (head_dim + 4) * 4 bytes * n_active above 16 MiB,
+ * or d_ff or (n_heads + 2 * n_kv_heads) * head_dim above 30840; other
+ * errors as spr_decode_step.
  */
 spr_status spr_decode_step_static_scratch(spr_model* m, int32_t n_active, const int32_t* slots, const int32_t* lens,
                                           int32_t* tok, float* logits, int32_t* retired);

@@ -40,18 +40,6 @@ struct AttnArgs {
   int split_start[kRows + 1];  // first flat split index of each row; [n_rows] = total
 };
 
-// Agent-coherent 8-byte store and load (relaxed device-scope atomics): a
-// work-group on any XCD reads the stored value once the storing wave's vmcnt
-// has drained, without a write-back of the storing XCD's L2.
-__device__ __forceinline__ void store_coherent2(float* p, float x, float y) {
-  const uint64_t v = static_cast<uint64_t>(__float_as_uint(x)) | (static_cast<uint64_t>(__float_as_uint(y)) << 32);
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 load_coherent2(const float* p) {
-  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_float2(__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
-}
-
 // Partials the last arriving split reads per round; the host keeps every
 // row's split count within one round.
 constexpr int kMergeChunk = 16;

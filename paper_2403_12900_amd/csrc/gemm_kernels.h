@@ -114,6 +114,30 @@ struct StreamRed {
 template <class P, int JT, int RT, int U, bool PK>
 using StreamStageOf = StreamStage<JT, RT, (U / 2 > 0 ? U / 2 : 1), StreamFrags<P, PK>::value>;
 
+// Split-K across work-groups.  With more than 8 rows every work-group reads
+// the whole activation of its K range, and O and down have only 256 tiles:
+// one tile per work-group means each CU re-reads the full activation (at 32
+// rows and two parts, four activation bytes per weight byte).  With S > 1
+// the S work-groups of a group of RT tiles each take a contiguous 1/S of the
+// K-blocks, so RT can be S times larger at the same work-group count and
+// each activation fragment feeds RT weight fragments.  Each work-group
+// publishes its partial sums (and the rows' partial sums of squares) with
+// agent-coherent stores and counts itself in; the last to arrive adds the S
+// partials in slice order -- the same order whichever arrives last, so the
+// result stays bitwise reproducible -- and runs the epilogue.  No work-group
+// waits on another.
+struct SplitK {
+  float* part;    // [group][slice][pair][64 lanes][2] floats
+  int32_t* cnt;   // [group] arrived slices; zero between launches
+};
+
+// Floats each lane publishes per slice (accumulators, then sums of squares),
+// rounded up to whole 8-byte pairs.
+template <int JT, int RT, bool kNorm>
+struct SplitKPairs {
+  static constexpr int value = (RT * JT * 4 + (kNorm ? JT : 0) + 1) / 2;
+};
+
 // The body of k_stream_gemm as a device function: the WAVES waves of the
 // calling work-group compute row tiles nt0 .. nt0 + RT - 1; red is LDS of
 // StreamRed<JT, WAVES, RT>::floats floats.  With WAVES > 1 every wave of the
@@ -121,18 +145,22 @@ using StreamStageOf = StreamStage<JT, RT, (U / 2 > 0 ? U / 2 : 1), StreamFrags<P
 // pipeline stages.  PK: packed rows (n_rows <= 8, JT = 1, two or three parts).
 // LP: parts per K-block of the activation record (at least P::parts; the
 // first P::parts are used).
-template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream, bool PK, int LP = P::parts>
+template <class P, int JT, int WAVES, class Epi, int RT, int U, bool kStream, bool PK, int LP = P::parts, int S = 1>
 __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, const uint4* __restrict__ X, int KB,
                                                   int Rp, int n_rows, const Epi& epi, int nt0, int wave, int lane,
                                                   float* red, StreamStageOf<P, JT, RT, U, PK>& s0,
-                                                  StreamStageOf<P, JT, RT, U, PK>& s1) {
+                                                  StreamStageOf<P, JT, RT, U, PK>& s1, const SplitK& sk = {},
+                                                  int slice = 0) {
   constexpr int PARTS = P::parts;
   static_assert(!PK || (JT == 1 && PARTS >= 2), "packed rows: one tile of at most 8 rows, two or three parts");
   static_assert(LP >= PARTS, "the record holds the parts used");
+  static_assert(S == 1 || !PK, "split-K is for unpacked rows");
   constexpr int XF = StreamFrags<P, PK>::value;
   constexpr int UH = U / 2 > 0 ? U / 2 : 1;
   using Stage = StreamStageOf<P, JT, RT, U, PK>;
-  const int kb0 = (KB * wave) / WAVES, kb1 = (KB * (wave + 1)) / WAVES;
+  // This work-group's K-blocks (its slice), split among its waves.
+  const int ks0 = (KB * slice) / S, ks1 = (KB * (slice + 1)) / S;
+  const int kb0 = ks0 + ((ks1 - ks0) * wave) / WAVES, kb1 = ks0 + ((ks1 - ks0) * (wave + 1)) / WAVES;
   // Gram accumulators per activation tile: hi.hi, then hi.lo (two parts) or
   // hi.mid, mid.mid, hi.lo (three parts); packed: (hi|lo)^2, or (hi|mid)^2
   // and (hi|mid).(lo|0).
@@ -294,6 +322,60 @@ __device__ __forceinline__ void stream_gemm_tiles(const uint4* __restrict__ W, c
       }
     }
   }
+  if constexpr (S > 1) {
+    // Publish this slice's partial, count it in; the last slice to arrive
+    // sums all S in slice order and goes on to the epilogue.
+    constexpr int NP = SplitKPairs<JT, RT, Epi::kNorm>::value;
+    float v[2 * NP];
+#pragma unroll
+    for (int i = 0; i < 2 * NP; ++i) v[i] = 0.f;
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int j = 0; j < JT; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[(t * JT + j) * 4 + c] = acc[t][j][c];
+    if constexpr (Epi::kNorm) {
+#pragma unroll
+      for (int j = 0; j < JT; ++j) v[RT * JT * 4 + j] = ssq[j];
+    }
+    const int g = nt0 / RT;
+    float* base = sk.part + static_cast<size_t>(g) * S * NP * 128 + 2 * lane;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) store_coherent2(base + (static_cast<size_t>(slice) * NP + i) * 128, v[2 * i], v[2 * i + 1]);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this slice's partial stores are complete
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    int last = 0;
+    if (lane == 0) last = __hip_atomic_fetch_add(sk.cnt + g, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+    if (!__builtin_amdgcn_readfirstlane(last)) return;
+    if (lane == 0) __hip_atomic_store(sk.cnt + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    float2 pv[S][NP];
+#pragma unroll
+    for (int q = 0; q < S; ++q)
+#pragma unroll
+      for (int i = 0; i < NP; ++i) pv[q][i] = load_coherent2(base + (static_cast<size_t>(q) * NP + i) * 128);
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      float2 a = pv[0][i];
+#pragma unroll
+      for (int q = 1; q < S; ++q) {
+        a.x += pv[q][i].x;
+        a.y += pv[q][i].y;
+      }
+      v[2 * i] = a.x;
+      v[2 * i + 1] = a.y;
+    }
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int j = 0; j < JT; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[t][j][c] = v[(t * JT + j) * 4 + c];
+    if constexpr (Epi::kNorm) {
+#pragma unroll
+      for (int j = 0; j < JT; ++j) ssq[j] = v[RT * JT * 4 + j];
+    }
+  }
   if constexpr (PK) {
     // Row c's parts 0 (and 2) are in column c, part 1 in column c + 8.
     const int src = (lane & 48) | ((lane + 8) & 15);
@@ -317,26 +399,42 @@ __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm(const uint4* __restr
                                                            threadIdx.x & 63, red, s0, s1);
 }
 
+// k_stream_gemm with split-K across work-groups (see SplitK): work-group i
+// takes slice i % S of group i / S, so the work-groups of one slice sit on
+// the same XCDs (work-groups go to the XCDs round robin) and each XCD's L2
+// holds only its slices' activations.
+template <class P, int JT, int WAVES, class Epi, int RT, int U, int S>
+__global__ __launch_bounds__(WAVES * 64) void k_stream_gemm_split(const uint4* __restrict__ W,
+                                                                  const uint4* __restrict__ X, int KB, int Rp,
+                                                                  int n_rows, Epi epi, SplitK sk) {
+  __shared__ float red[StreamRed<JT, WAVES, RT>::floats];
+  StreamStageOf<P, JT, RT, U, false> s0, s1;
+  stream_gemm_tiles<P, JT, WAVES, Epi, RT, U, true, false, P::parts, S>(
+      W, X, KB, Rp, n_rows, epi, (blockIdx.x / S) * RT, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
+      threadIdx.x & 63, red, s0, s1, sk, blockIdx.x % S);
+}
+
 // QKV projection of bf16 models over a three-part record: query tiles (the
 // first q_tiles, a multiple of RT) take its first two parts -- hi and mid are
 // the two-part form of the same values -- and key and value tiles, which are
 // rounded into the bf16 cache, all three.  The branch is uniform per
 // work-group.
-template <int JT, int WAVES, class Epi, int RT, int U2, int U3, bool PK>
+// With S > 1, split-K across work-groups as in k_stream_gemm_split.
+template <int JT, int WAVES, class Epi, int RT, int U2, int U3, bool PK, int S = 1>
 __global__ __launch_bounds__(WAVES * 64) void k_stream_gemm_qkv(const uint4* __restrict__ W,
                                                                 const uint4* __restrict__ X, int KB, int Rp,
-                                                                int n_rows, Epi epi, int q_tiles) {
+                                                                int n_rows, Epi epi, int q_tiles, SplitK sk = {}) {
   __shared__ float red[StreamRed<JT, WAVES, RT>::floats];
-  const int nt0 = blockIdx.x * RT;
+  const int nt0 = (blockIdx.x / S) * RT, slice = blockIdx.x % S;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (nt0 < q_tiles) {
     StreamStageOf<BF16, JT, RT, U2, PK> s0, s1;
-    stream_gemm_tiles<BF16, JT, WAVES, Epi, RT, U2, true, PK, 3>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane, red,
-                                                                 s0, s1);
+    stream_gemm_tiles<BF16, JT, WAVES, Epi, RT, U2, true, PK, 3, S>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane, red,
+                                                                    s0, s1, sk, slice);
   } else {
     StreamStageOf<BF16x3, JT, RT, U3, PK> s0, s1;
-    stream_gemm_tiles<BF16x3, JT, WAVES, Epi, RT, U3, true, PK>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane, red,
-                                                                s0, s1);
+    stream_gemm_tiles<BF16x3, JT, WAVES, Epi, RT, U3, true, PK, 3, S>(W, X, KB, Rp, n_rows, epi, nt0, wave, lane,
+                                                                      red, s0, s1, sk, slice);
   }
 }
 

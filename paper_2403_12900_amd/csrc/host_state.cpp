@@ -114,15 +114,38 @@ Layout layout(const Dims& d) {
   l.off_act0 = take(l.act_bytes);
   l.off_act1 = take(l.act_bytes);
   l.off_q = take(static_cast<size_t>(kPrefillRows) * d.H * d.hd * sizeof(float));
-  l.off_part = take(static_cast<size_t>(kMaxSplits) * d.H * (d.hd + 4) * sizeof(float));
-  // Split arrival counters of decode attention, one per (row, KV head); zero between launches.
-  l.off_cnt = take(static_cast<size_t>(kMaxRows) * d.Hkv * sizeof(int32_t));
+  // Partials of decode attention's KV splits, or of the projections' split-K
+  // slices (never both in one launch).
+  const SplitNeed sn = split_need(d);
+  l.part_floats = std::max(static_cast<size_t>(kMaxSplits) * d.H * (d.hd + 4), sn.part_floats);
+  l.off_part = take(l.part_floats * sizeof(float));
+  // Arrival counters: decode attention's, one per (row, KV head), or the
+  // split-K groups'; zero between launches.
+  l.n_cnt = std::max(kMaxRows * d.Hkv, sn.counters);
+  l.off_cnt = take(static_cast<size_t>(l.n_cnt) * sizeof(int32_t));
   l.off_amax = take(static_cast<size_t>(d.nt_lm) * kMaxRows * 2 * sizeof(float));
   l.off_prow = take(static_cast<size_t>(kPrefillRows) * 4 * sizeof(int32_t));
   l.off_ptile = take(static_cast<size_t>(kPrefillTiles) * 4 * sizeof(int32_t));
   l.off_rs = take(static_cast<size_t>(kPrefillRows) * sizeof(float));
   l.total = off;
   return l;
+}
+
+SplitNeed split_need(const Dims& d) {
+  // The largest partials come at 32 rows (two 16-row activation tiles): per
+  // group and slice, 64 lanes x (rt x 2 x 4 accumulators, plus 2 sums of
+  // squares for the normed projections) floats in whole pairs.
+  auto need = [](int nt, SplitShape sh, bool norm) {
+    const size_t pairs = (sh.rt * 2 * 4 + (norm ? 2 : 0) + 1) / 2;
+    return SplitNeed{static_cast<size_t>(nt / sh.rt) * sh.s * pairs * 128, nt / sh.rt};
+  };
+  SplitNeed out{0, 0};
+  for (const SplitNeed& n : {need(d.nt_o, kSplitO, false), need(d.nt_2, kSplitO, false),
+                             need(d.nt_13, kSplitGU, true), need(d.nt_qkv, kSplitQKV, true)}) {
+    out.part_floats = std::max(out.part_floats, n.part_floats);
+    out.counters = std::max(out.counters, n.counters);
+  }
+  return out;
 }
 
 void SlotTable::init(const Dims& d) {

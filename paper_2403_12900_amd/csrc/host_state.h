@@ -36,11 +36,28 @@ struct Dims {
   float rope_base, eps;
 };
 
+// Split-K shapes of the decode projections past 8 rows (16-row tiles per
+// group, K slices): O and down, gate/up, QKV.
+struct SplitShape {
+  int rt, s;
+};
+constexpr SplitShape kSplitO{2, 4}, kSplitGU{4, 2}, kSplitQKV{4, 4};
+
+// Bounds on what the split-K launches of any decode pass of the model use:
+// partial-sum floats and arrival counters.
+struct SplitNeed {
+  size_t part_floats;
+  int counters;
+};
+SplitNeed split_need(const Dims& d);
+
 struct Layout {
   size_t wqkv, wo, w13, w2;        // per-layer strides of the tiled weights (bytes)
   size_t off_wqkv, off_wo, off_w13, off_w2, off_wlm, off_emb;
   size_t off_rope, off_kc, off_vc, kv_layer_stride, off_bt;
   size_t off_x, off_act0, off_act1, act_bytes, off_q, off_part, off_cnt, off_amax;
+  size_t part_floats;              // capacity of the partials region (attention splits, split-K)
+  int n_cnt;                       // capacity of the counters region
   size_t off_prow, off_ptile, off_rs;  // prefill chunk: row table, query tiles, RMSNorm scales
   size_t total;
 };

@@ -26,6 +26,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "attn_kernels.h"
@@ -42,14 +43,14 @@ static_assert(spr::kMaxRows == sprk::kRows, "decode pass size");
 
 // Scratch of spr_decode_step_static_scratch: a fixed array in device memory,
 // one per device that loads the library, held until the process ends.
-// Regions: attention split partials, split arrival counters, LM-head greedy
-// candidates.  Host code never passes the array's name to a kernel (on the
+// Regions: split partials (of attention, or of the projections' split-K
+// slices), arrival counters, LM-head greedy candidates.  Host code never passes the array's name to a kernel (on the
 // host it is only a stand-in symbol): it resolves the array's device address
 // once per device at init (static_scratch_address) and passes that.
-constexpr size_t kStaticPartBytes = size_t{8} << 20;
+constexpr size_t kStaticPartBytes = size_t{16} << 20;
 constexpr size_t kStaticCntBytes = size_t{64} << 10;
 constexpr size_t kStaticAmaxBytes = (size_t{8} << 20) - kStaticCntBytes;
-constexpr size_t kStaticScratchBytes = kStaticPartBytes + kStaticCntBytes + kStaticAmaxBytes;  // 16 MiB
+constexpr size_t kStaticScratchBytes = kStaticPartBytes + kStaticCntBytes + kStaticAmaxBytes;  // 24 MiB
 __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 struct spr_model {
@@ -205,12 +206,27 @@ struct DecodeScratch {
   int32_t* cnt;
   float2* amax;
   int max_splits;
+  size_t part_floats;  // capacity of part
+  int n_cnt;           // capacity of cnt
 };
 
 DecodeScratch workspace_scratch(const spr_model* m) {
   Ptrs p{m->ws, &m->lay};
-  return DecodeScratch{p.part(), p.cnt(), p.amax(), spr::kMaxSplits};
+  return DecodeScratch{p.part(), p.cnt(), p.amax(), spr::kMaxSplits, m->lay.part_floats, m->lay.n_cnt};
 }
+
+// Room for split-K partials and arrival counters (see SplitK): the regions of
+// the attention split partials and counters, which hold what any pass's
+// split-K launches need (spr::split_need) and which every launch that uses
+// them leaves zero.
+struct SplitRoom {
+  float* part = nullptr;  // null: no split-K
+  int32_t* cnt = nullptr;
+  size_t part_floats = 0;
+  int n_cnt = 0;
+};
+
+SplitRoom split_room(const DecodeScratch& sc) { return SplitRoom{sc.part, sc.cnt, sc.part_floats, sc.n_cnt}; }
 
 template <class P>
 spr_status init_weights(spr_model* m) {
@@ -253,19 +269,65 @@ struct RowSet {
   int hist_idx[kRows];  // token-history index of the row's token, -1 = none
 };
 
+// Whether an epilogue is a residual update (O and down).
+template <class E>
+struct IsResid : std::false_type {};
+template <class F>
+struct IsResid<EpiResid<F>> : std::true_type {};
+
+// Split-K pays (see SplitK) once a work-group's activation range holds at
+// least this many K-block parts per 16-row tile (at two parts, 384 KiB of
+// activations per work-group at 16 rows): measured on the 7B projections at
+// 12-32 rows, it is then 1-7 us faster per launch; below (O and gate/up at
+// 9-16 rows) the slices' publication costs more than it saves.
+constexpr int kSplitMinParts = 384;
+
+// Split-K launch (see SplitK) of S slices per group of RT tiles, WAVES waves
+// per work-group; false (nothing launched) when the tiles do not divide into
+// groups or the room is too small.
+template <class P, int JT, int WAVES, int RT, int S, int U, class Epi>
+bool launch_split(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi,
+                  const SplitRoom& room) {
+  const int groups = NT / RT;
+  if (room.part == nullptr || NT % RT != 0 || groups > room.n_cnt ||
+      static_cast<size_t>(groups) * S * SplitKPairs<JT, RT, Epi::kNorm>::value * 128 > room.part_floats)
+    return false;
+  k_stream_gemm_split<P, JT, WAVES, Epi, RT, U, S><<<groups * S, WAVES * 64, 0, st>>>(
+      w, x, KB, 16 * JT, epi.n_rows, epi, SplitK{room.part, room.cnt});
+  return true;
+}
+
 // Launch shape of a projection, from sweeps over the 7B projection shapes on
 // MI355X at 1..32 rows:
+//   * at 9..32 rows, where a work-group's activation range holds at least
+//     kSplitMinParts K-block parts per tile: split-K across work-groups (for
+//     the 7B shapes down at 9..32 rows, O and gate/up at 17..32); never the
+//     LM head;
 //   * wide projections (>= 1024 16-row tiles: gate/up, LM head) at up to 32
 //     rows: one-wave work-groups, each streaming two whole tiles over the
 //     full K -- long contiguous streams and no cross-wave reduction;
-//   * projections of 512..1023 tiles (QKV) at 17..64 rows: four waves split
-//     K for two tiles, so each activation fragment feeds two weight fragments;
+//   * projections of 512..1023 tiles at 17..64 rows: four waves split K for
+//     two tiles, so each activation fragment feeds two weight fragments;
 //   * everything else: four waves split K for one tile.
 // PK: packed rows (at most 8 rows, two activation parts per fragment).
 template <class P, int JT, bool PK, class Epi>
-void launch_gemm_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi) {
+void launch_gemm_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi,
+                       const SplitRoom& room) {
   const int Rp = 16 * JT, n = epi.n_rows;
   constexpr int XF = StreamFrags<P, PK>::value;  // activation fragments per K-block and tile
+  if constexpr (!PK && JT <= 2) {
+    // Past 8 rows, with enough activation bytes per work-group: split-K.
+    // Shapes from sweeps of the 7B projections at 12-32 rows.
+    if (KB * JT * P::parts >= kSplitMinParts) {
+      if constexpr (IsResid<Epi>::value) {
+        // O and down: two tiles per group, four slices of two waves.
+        if (launch_split<P, JT, 2, spr::kSplitO.rt, spr::kSplitO.s, 4>(st, NT, w, x, KB, epi, room)) return;
+      } else if constexpr (std::is_same_v<Epi, EpiSwiGLU<P>>) {
+        // gate/up: four tiles per group, two one-wave slices.
+        if (launch_split<P, JT, 1, spr::kSplitGU.rt, spr::kSplitGU.s, 4>(st, NT, w, x, KB, epi, room)) return;
+      }
+    }
+  }
   if constexpr (JT <= 2) {
     if (NT >= 1024 && NT % 2 == 0) {
       constexpr int U = XF == 3 ? (JT == 1 ? 4 : 2) : (JT == 1 ? 8 : 4);
@@ -284,12 +346,28 @@ void launch_gemm_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, i
 }
 
 // QKV of bf16 models (three-part input, see k_stream_gemm_qkv): four waves
-// splitting K, one tile per work-group with packed rows (at most 8), else two
-// (measured on the 7B shape at 16 rows: 1.2% less decode-step time than one).
+// splitting K of one tile per work-group with packed rows (at most 8); at
+// 9..32 rows split-K across work-groups; without room for its partials, two
+// tiles per work-group (measured on the 7B shape at 16 rows: 1.2% less
+// decode-step time than one).
 template <int JT, bool PK, class Epi>
-void launch_qkv_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi) {
+void launch_qkv_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, int KB, const Epi& epi,
+                      const SplitRoom& room) {
   const int Rp = 16 * JT, n = epi.n_rows;
   const int q_tiles = epi.H * epi.hd / 16;
+  if constexpr (!PK && JT <= 2) {
+    // Past 8 rows: split-K, four tiles per group, four slices of two waves
+    // (9-16 rows) or one (17-32 rows); from sweeps of the 7B QKV projection.
+    constexpr int RT = spr::kSplitQKV.rt, S = spr::kSplitQKV.s, WV = JT == 1 ? 2 : 1;
+    const int groups = NT / RT;
+    if (KB * JT * 3 >= kSplitMinParts && room.part != nullptr && NT % RT == 0 && q_tiles % RT == 0 &&
+        groups <= room.n_cnt &&
+        static_cast<size_t>(groups) * S * SplitKPairs<JT, RT, true>::value * 128 <= room.part_floats) {
+      k_stream_gemm_qkv<JT, WV, Epi, RT, 4, 4, false, S>
+          <<<groups * S, WV * 64, 0, st>>>(w, x, KB, Rp, n, epi, q_tiles, SplitK{room.part, room.cnt});
+      return;
+    }
+  }
   if constexpr (!PK && JT <= 4) {
     if (NT % 2 == 0 && q_tiles % 2 == 0) {
       k_stream_gemm_qkv<JT, 4, Epi, 2, StreamDepth<2 * JT * 2>::value, StreamDepth<2 * JT * 3>::value, false>
@@ -307,21 +385,22 @@ void launch_qkv_shape(hipStream_t st, int NT, const uint4* w, const uint4* x, in
 }
 
 template <class P, class Epi>
-spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int KB, int JT, const Epi& epi) {
+spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int KB, int JT, const Epi& epi,
+                       const SplitRoom& room = {}) {
   const uint4* w = reinterpret_cast<const uint4*>(W);
   const uint4* x = reinterpret_cast<const uint4*>(X);
   if constexpr (P::parts == 3) {
     switch (JT) {
       case 1:
         if (epi.n_rows <= 8) {
-          launch_qkv_shape<1, true>(m->st, NT, w, x, KB, epi);
+          launch_qkv_shape<1, true>(m->st, NT, w, x, KB, epi, room);
         } else {
-          launch_qkv_shape<1, false>(m->st, NT, w, x, KB, epi);
+          launch_qkv_shape<1, false>(m->st, NT, w, x, KB, epi, room);
         }
         break;
-      case 2: launch_qkv_shape<2, false>(m->st, NT, w, x, KB, epi); break;
-      case 4: launch_qkv_shape<4, false>(m->st, NT, w, x, KB, epi); break;
-      case 8: launch_qkv_shape<8, false>(m->st, NT, w, x, KB, epi); break;
+      case 2: launch_qkv_shape<2, false>(m->st, NT, w, x, KB, epi, room); break;
+      case 4: launch_qkv_shape<4, false>(m->st, NT, w, x, KB, epi, room); break;
+      case 8: launch_qkv_shape<8, false>(m->st, NT, w, x, KB, epi, room); break;
       default:
         return fail(SPR_ERR_INVALID_ARG, "internal: unsupported row-tile count");
     }
@@ -332,15 +411,15 @@ spr_status launch_gemm(spr_model* m, int NT, const char* W, const char* X, int K
     case 1:
       if constexpr (P::parts >= 2) {
         if (epi.n_rows <= 8) {
-          launch_gemm_shape<P, 1, true>(m->st, NT, w, x, KB, epi);
+          launch_gemm_shape<P, 1, true>(m->st, NT, w, x, KB, epi, room);
           break;
         }
       }
-      launch_gemm_shape<P, 1, false>(m->st, NT, w, x, KB, epi);
+      launch_gemm_shape<P, 1, false>(m->st, NT, w, x, KB, epi, room);
       break;
-    case 2: launch_gemm_shape<P, 2, false>(m->st, NT, w, x, KB, epi); break;
-    case 4: launch_gemm_shape<P, 4, false>(m->st, NT, w, x, KB, epi); break;
-    case 8: launch_gemm_shape<P, 8, false>(m->st, NT, w, x, KB, epi); break;
+    case 2: launch_gemm_shape<P, 2, false>(m->st, NT, w, x, KB, epi, room); break;
+    case 4: launch_gemm_shape<P, 4, false>(m->st, NT, w, x, KB, epi, room); break;
+    case 8: launch_gemm_shape<P, 8, false>(m->st, NT, w, x, KB, epi, room); break;
     default:
       return fail(SPR_ERR_INVALID_ARG, "internal: unsupported row-tile count");
   }
@@ -456,6 +535,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
   for (int r = 0; r < n; ++r)
     while (ceil_div((rs.pos[r] + 1 + 15) / 16, 4 * bpw) > kMergeChunk) ++bpw;
 
+  const SplitRoom room = split_room(sc);
   spr_status st;
   for (int l = 0; l < d.L; ++l) {
     {
@@ -473,7 +553,7 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
       e.bt = p.bt();
       e.rope = p.rope();
       e.rows = sp;
-      if ((st = launch_gemm<QKVIn<P>>(m, d.nt_qkv, p.wqkv(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
+      if ((st = launch_gemm<QKVIn<P>>(m, d.nt_qkv, p.wqkv(l), p.act(0), d.kb_d, JT, e, room)) != SPR_OK) return st;
     }
     {
       const AttnArgs a = attention_args<P, KP>(m, l, rs, sp, Rp, bpw, p.act(1), sc);
@@ -482,18 +562,18 @@ spr_status forward(spr_model* m, const RowSet& rs, const int32_t* tok_in, int32_
     }
     {
       EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      if ((st = launch_gemm<P>(m, d.nt_o, p.wo(l), p.act(1), d.kb_o, JT, e)) != SPR_OK) return st;
+      if ((st = launch_gemm<P>(m, d.nt_o, p.wo(l), p.act(1), d.kb_o, JT, e, room)) != SPR_OK) return st;
     }
     {
       EpiSwiGLU<P> e{n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(1))};
-      if ((st = launch_gemm<P>(m, d.nt_13, p.w13(l), p.act(0), d.kb_d, JT, e)) != SPR_OK) return st;
+      if ((st = launch_gemm<P>(m, d.nt_13, p.w13(l), p.act(0), d.kb_d, JT, e, room)) != SPR_OK) return st;
     }
     if (l + 1 < d.L) {  // the new residual is the next layer's QKV input
       EpiResid<QKVIn<P>> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e)) != SPR_OK) return st;
+      if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e, room)) != SPR_OK) return st;
     } else {            // ... or the LM head's
       EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e)) != SPR_OK) return st;
+      if ((st = launch_gemm<P>(m, d.nt_2, p.w2(l), p.act(1), d.kb_f, JT, e, room)) != SPR_OK) return st;
     }
   }
   {
@@ -528,21 +608,22 @@ template <class P>
 spr_status launch_projection(spr_model* m, int projection, int layer, int n) {
   const spr::Dims& d = m->d;
   Ptrs p{m->ws, &m->lay};
+  const SplitRoom room = split_room(workspace_scratch(m));
   const int JT = n <= 16 ? 1 : n <= 32 ? 2 : n <= 64 ? 4 : 8;
   const int Rp = 16 * JT;
   using E = typename P::elem;
   switch (projection) {
     case 1: {
       EpiResid<P> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      return launch_gemm<P>(m, d.nt_o, p.wo(layer), p.act(1), d.kb_o, JT, e);
+      return launch_gemm<P>(m, d.nt_o, p.wo(layer), p.act(1), d.kb_o, JT, e, room);
     }
     case 2: {
       EpiSwiGLU<P> e{n, d.d, Rp, d.eps, reinterpret_cast<E*>(p.act(1))};
-      return launch_gemm<P>(m, d.nt_13, p.w13(layer), p.act(0), d.kb_d, JT, e);
+      return launch_gemm<P>(m, d.nt_13, p.w13(layer), p.act(0), d.kb_d, JT, e, room);
     }
     case 3: {  // as in every layer but the last
       EpiResid<QKVIn<P>> e{n, d.d, Rp, p.x(), reinterpret_cast<E*>(p.act(0))};
-      return launch_gemm<P>(m, d.nt_2, p.w2(layer), p.act(1), d.kb_f, JT, e);
+      return launch_gemm<P>(m, d.nt_2, p.w2(layer), p.act(1), d.kb_f, JT, e, room);
     }
     default: {
       EpiLogits<P> e{};
@@ -1057,11 +1138,15 @@ spr_status spr_decode_step_static_scratch(spr_model* m, int32_t n_active, const 
   const spr::Dims& d = m->d;
   const size_t per_split = static_cast<size_t>(d.H) * (d.hd + 4) * sizeof(float);
   const int max_splits = static_cast<int>(std::min<size_t>(spr::kMaxSplits, kStaticPartBytes / per_split));
+  const spr::SplitNeed sn = spr::split_need(d);
   if (static_cast<size_t>(spr::kMaxRows) * d.Hkv * sizeof(int32_t) > kStaticCntBytes ||
-      static_cast<size_t>(d.nt_lm) * spr::kMaxRows * sizeof(float2) > kStaticAmaxBytes || max_splits < n_active)
-    return fail(SPR_ERR_INVALID_ARG, "decode_step_static_scratch: the model or batch exceeds the 16 MiB static "
-                                     "scratch (at most 128 KV heads, vocab <= 130048, and n_heads * (head_dim + 4) "
-                                     "* 4 * n_active <= 8 MiB)");
+      static_cast<size_t>(d.nt_lm) * spr::kMaxRows * sizeof(float2) > kStaticAmaxBytes || max_splits < n_active ||
+      sn.part_floats * sizeof(float) > kStaticPartBytes ||
+      static_cast<size_t>(sn.counters) * sizeof(int32_t) > kStaticCntBytes)
+    return fail(SPR_ERR_INVALID_ARG, "decode_step_static_scratch: the model or batch exceeds the 24 MiB static "
+                                     "scratch (at most 128 KV heads, vocab <= 130048, n_heads * (head_dim + 4) "
+                                     "* 4 * n_active <= 16 MiB, d_ff <= 30840 and (n_heads + 2 * n_kv_heads) * "
+                                     "head_dim <= 30840)");
   std::string err;
   if ((st = m->tab.check_decode(n_active, slots, lens, &err)) != SPR_OK) return fail(st, err);
   RowSet rs;
@@ -1076,10 +1161,14 @@ spr_status spr_decode_step_static_scratch(spr_model* m, int32_t n_active, const 
   }
   DecodeScratch sc{reinterpret_cast<float*>(m->static_scratch),
                    reinterpret_cast<int32_t*>(m->static_scratch + kStaticPartBytes),
-                   reinterpret_cast<float2*>(m->static_scratch + kStaticPartBytes + kStaticCntBytes), max_splits};
-  // Every call shares the array: the split counters must start at zero (a
-  // fill kernel, which a graph capture may record).
-  const int ncnt = n_active * d.Hkv;
+                   reinterpret_cast<float2*>(m->static_scratch + kStaticPartBytes + kStaticCntBytes),
+                   max_splits,
+                   kStaticPartBytes / sizeof(float),
+                   static_cast<int>(kStaticCntBytes / sizeof(int32_t))};
+  // Every call shares the array: the attention split counters and the
+  // projections' split-K counters must start at zero (a fill kernel, which a
+  // graph capture may record).
+  const int ncnt = std::max(n_active * d.Hkv, spr::split_need(d).counters);
   k_zero_i32<<<ceil_div(ncnt, 256), 256, 0, m->st>>>(sc.cnt, ncnt);
   SPR_LAUNCHED(m, "k_zero_i32");
   if ((st = forward_any(m, rs, tok, tok, logits, nullptr, sc)) != SPR_OK) return st;

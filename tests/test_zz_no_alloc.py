@@ -1,8 +1,9 @@
 """spr_decode_step_static_scratch against spr_decode_step, through the C ABI (needs an MI355X).
 
-The static-scratch variant is for callers that cannot allocate: its attention
-split partials, split counters and greedy candidates live in the library's
-fixed per-device array instead of the model's workspace.  It must give the
+The static-scratch variant is for callers that cannot allocate: its split
+partials (attention's, and past 8 rows the projections' split-K slices),
+arrival counters and greedy candidates live in the library's fixed
+per-device array instead of the model's workspace.  It must give the
 same tokens and the same logits as spr_decode_step on the same inputs, on
 consecutive calls that share the array, the second with a smaller batch (the
 array keeps the first call's contents).
@@ -22,6 +23,9 @@ CASES = {
                                   vocab=1000), [700, 301, 455, 16, 640, 333]),
     # The benchmarked model's shape: 2000 LM-head tiles of greedy candidates in the scratch.
     "llama2_7b": (CONFIGS["c3"].model, [517, 140, 1033, 64]),
+    # 24 and then 12 rows: the projections' split-K partials and counters in the scratch too.
+    "llama2_7b_24_rows": (CONFIGS["c3"].model, [517, 140, 1033, 64, 300, 17, 250, 96, 401, 33, 129, 77,
+                                                 610, 45, 160, 288, 71, 512, 20, 199, 345, 88, 131, 256]),
 }
 
 
