@@ -123,6 +123,12 @@ TOY_CASES = {
     "bf16_mha32_splits_fit_resident": (
         ModelConfig(n_layers=1, d_model=256, n_heads=32, n_kv_heads=32, head_dim=64, d_ff=128, vocab=300),
         [140 + (i % 5) for i in range(24)], [3] * 24),
+    # Split-K past 8 rows with slices of unequal length: d = 4160 (130 K-blocks: QKV and O slices
+    # of 32 and 33) and d_ff = 6208 (194: down slices of 48 and 49).  At 17-20 rows QKV, O, gate/up
+    # and down split; at 9-16 QKV and down; at 1-8 none.  13 query heads per KV head.
+    "bf16_split_k_uneven_slices": (
+        ModelConfig(n_layers=1, d_model=4160, n_heads=65, n_kv_heads=5, head_dim=64, d_ff=6208, vocab=600),
+        [(5 * i) % 23 + 1 for i in range(20)], [2] * 4 + [3] * 4 + [5, 6] * 6),
     # The slot limit: 64 requests, so the first decode pass has 64 rows (four row tiles); later
     # passes shrink through two and one row tiles as requests retire.
     "bf16_batch64_max_slots": (
@@ -271,13 +277,14 @@ def test_rewind_regenerates_identically():
     dm.close()
 
 
-@pytest.mark.parametrize("case", ["bf16_gqa4_hd128_wide_o", "bf16_gqa4_hd128_long_context"])
+@pytest.mark.parametrize("case", ["bf16_gqa4_hd128_wide_o", "bf16_gqa4_hd128_long_context",
+                                  "bf16_split_k_uneven_slices"])
 def test_repeat_runs_are_bitwise_identical(case):
     """Two runs of the same batch give bitwise equal tokens and logits at every step: cross-wave and
-    cross-split reductions have a fixed order (the split merge counts arrivals with an atomic, but the
+    cross-split reductions have a fixed order (the split merges count arrivals with an atomic, but the
     last split reads every partial in split order).  The first case passes through 20, 15 and 5 rows
     (two-tile, one-tile and packed-row projections), the second through attention splits over a
-    1690-position context."""
+    1690-position context, the third through the projections' split-K slices."""
     m, plens, stops = TOY_CASES[case]
     say(f"repeat runs {case}")
     rng = np.random.default_rng(11)
